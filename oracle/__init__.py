@@ -1,0 +1,16 @@
+"""fp64 CPU oracle for the token log-probability path and its mismatch statistics.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path may import, call or run
+anything in this package; only the tests, the smoke check and the benchmark's
+CPU-baseline leg use it. It shares no code with the HIP library: it reads the
+raw bf16 bit patterns of the inputs, widens them exactly to fp64 and computes
+each quantity straight from its definition.
+
+Parity status (each function's own docstring names its pins):
+
+* ``logprobs``      pinned (closed forms, brute force, library routines).
+* ``mismatch``      pinned (Table 1 of the paper, closed forms, series).
+"""
+
+from .logprobs import bf16_to_f64, logits, logprobs  # noqa: F401
+from .mismatch import mismatch  # noqa: F401

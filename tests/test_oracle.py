@@ -1,0 +1,303 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle itself.
+
+Each test fixes the oracle to something independent: exact rational
+arithmetic, a closed form, a library routine (torch's bf16 widening, scipy's
+log_softmax and entropy), an identity between two of its outputs that a
+dropped term or a wrong index would break, or the values printed in Table 1.
+"""
+
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+import scipy.stats
+import torch
+
+import oracle
+from workload import bf16_bits
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _bits(x):
+    """fp32/fp64 array -> bf16 bit patterns (torch RNE cast)."""
+    return bf16_bits(torch.as_tensor(np.asarray(x, dtype=np.float32)).to(torch.bfloat16))
+
+
+def _rand_bits(shape, seed, scale=1.0):
+    rng = np.random.default_rng(seed)
+    return _bits(rng.standard_normal(shape) * scale)
+
+
+# ---------------------------------------------------------------- bf16 widening
+
+def test_bf16_widening_matches_torch():
+    rng = np.random.default_rng(0)
+    vals = np.concatenate([rng.standard_normal(1000) * 10.0 ** rng.integers(-40, 38, 1000),
+                           [0.0, -0.0, np.inf, -np.inf, 1e-39, -1e-40, 3.0e38]]).astype(np.float32)
+    t = torch.as_tensor(vals).to(torch.bfloat16)
+    ref = t.to(torch.float64).numpy()
+    got = oracle.bf16_to_f64(bf16_bits(t))
+    np.testing.assert_array_equal(got, ref)
+    nan_bits = np.array([0x7FC0, 0xFFC1], dtype=np.uint16)
+    assert np.isnan(oracle.bf16_to_f64(nan_bits)).all()
+
+
+# ---------------------------------------------------------------- logits
+
+def test_logits_exact_rational():
+    """z = (h . w) / tau against exact rational dot products."""
+    T, d, V = 3, 16, 5
+    hb = _rand_bits((T, d), 1)
+    wb = _rand_bits((V, d), 2, 0.3)
+    tau = 0.7
+    z = oracle.logits(hb, wb, tau)
+    hf = oracle.bf16_to_f64(hb)
+    wf = oracle.bf16_to_f64(wb)
+    for i in range(T):
+        for v in range(V):
+            exact = sum(Fraction(hf[i, k]) * Fraction(wf[v, k]) for k in range(d)) / Fraction(tau)
+            assert abs(Fraction(z[i, v]) - exact) <= abs(exact) * Fraction(1, 2 ** 50) + Fraction(1, 2 ** 1000)
+
+
+def test_logits_vocab_chunking_is_exact_split():
+    hb = _rand_bits((4, 32), 3)
+    wb = _rand_bits((50, 32), 4)
+    a = oracle.logits(hb, wb, 1.0, vocab_chunk=7)
+    b = oracle.logits(hb, wb, 1.0, vocab_chunk=50)
+    np.testing.assert_allclose(a, b, rtol=1e-15, atol=1e-15)
+    assert a.shape == (4, 50)
+
+
+# ---------------------------------------------------------------- closed forms
+
+@pytest.mark.parametrize("V", [1, 2, 7, 4096, 151936])
+def test_uniform_row(V):
+    """h = 0: every logit is 0, so logp = -log V and H = log V."""
+    d = 32
+    hb = _bits(np.zeros((2, d)))
+    wb = _rand_bits((V, d), 5)
+    tok = np.array([0, V - 1])
+    lp, H = oracle.logprobs(hb, wb, tok, 1.0)
+    np.testing.assert_allclose(lp, -math.log(V), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(H, math.log(V), rtol=0, atol=1e-12)
+
+
+def test_identical_vocab_rows_uniform():
+    """All w_v equal (h nonzero): uniform distribution again."""
+    V, d = 300, 64
+    row = _rand_bits((1, d), 6)
+    wb = np.repeat(row, V, axis=0)
+    hb = _rand_bits((3, d), 7)
+    lp, H = oracle.logprobs(hb, wb, np.array([0, 17, 299]), 1.0)
+    np.testing.assert_allclose(lp, -math.log(V), atol=1e-12)
+    np.testing.assert_allclose(H, math.log(V), atol=1e-12)
+
+
+def test_single_token_vocab():
+    hb = _rand_bits((4, 32), 8)
+    wb = _rand_bits((1, 32), 9)
+    lp, H = oracle.logprobs(hb, wb, np.zeros(4, dtype=np.int64), 0.9)
+    np.testing.assert_array_equal(lp, 0.0)
+    np.testing.assert_allclose(H, 0.0, atol=1e-15)
+
+
+def _planted(zrows, tau=1.0):
+    """h = e_0, W[:, 0] = z values (exact in bf16): logits equal z / tau exactly."""
+    zrows = np.asarray(zrows, dtype=np.float64)
+    T, V = zrows.shape
+    d = 32
+    assert T == 1
+    h = np.zeros((1, d)); h[0, 0] = 1.0
+    w = np.zeros((V, d)); w[:, 0] = zrows[0]
+    hb, wb = _bits(h), _bits(w)
+    np.testing.assert_array_equal(oracle.bf16_to_f64(wb)[:, 0], zrows[0])  # exact in bf16
+    return hb, wb
+
+
+@pytest.mark.parametrize("z0,z1", [(0.0, 0.0), (1.5, -0.25), (-3.0, 5.0), (20.0, -20.0)])
+def test_two_token_vocab_closed_form(z0, z1):
+    hb, wb = _planted([[z0, z1]])
+    for tok in (0, 1):
+        lp, H = oracle.logprobs(hb, wb, np.array([tok]), 1.0)
+        dz = (z0 - z1) if tok == 0 else (z1 - z0)
+        exp_lp = -math.log1p(math.exp(-dz)) if dz > -700 else dz
+        p = 1.0 / (1.0 + math.exp(-(z0 - z1)))
+        exp_H = -sum(q * math.log(q) for q in (p, 1.0 - p) if q > 0)
+        assert abs(lp[0] - exp_lp) <= 1e-13
+        assert abs(H[0] - exp_H) <= 1e-13
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("tau", [1.0, 0.7, 3.0])
+def test_planted_logits_vs_scipy(seed, tau):
+    """Known logit vector: compare with scipy's log_softmax and entropy."""
+    rng = np.random.default_rng(seed)
+    V = 97
+    z = oracle.bf16_to_f64(_bits(rng.standard_normal(V) * 4))
+    hb, wb = _planted(z[None, :])
+    ref_lsm = scipy.special.log_softmax(z / tau)
+    ref_H = scipy.stats.entropy(scipy.special.softmax(z / tau))
+    for tok in (0, 13, 96):
+        lp, H = oracle.logprobs(hb, wb, np.array([tok]), tau)
+        assert abs(lp[0] - ref_lsm[tok]) <= 1e-12
+        assert abs(H[0] - ref_H) <= 1e-12
+
+
+def test_one_hot_dominant_row():
+    """The token's logit exceeds every other by >= 100: logp ~ 0 and H ~ 0."""
+    V = 64
+    z = np.full(V, -50.0); z[11] = 60.0
+    hb, wb = _planted(z[None, :])
+    lp, H = oracle.logprobs(hb, wb, np.array([11]), 1.0)
+    assert -1e-40 <= lp[0] <= 0.0
+    assert 0.0 <= H[0] <= 1e-40
+    lp_other, _ = oracle.logprobs(hb, wb, np.array([3]), 1.0)
+    assert abs(lp_other[0] - (-110.0)) <= 1e-12
+
+
+# ---------------------------------------------------------------- identities
+
+def _tiny(T=5, V=40, d=32, seed=11, scale=1.0):
+    return _rand_bits((T, d), seed, scale), _rand_bits((V, d), seed + 1, 0.3)
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.5])
+def test_probabilities_sum_to_one_and_entropy_identity(tau):
+    """For each row: sum_v exp(logp(v)) = 1 and H = -sum_v p_v logp(v), where
+    logp(v) is the oracle's own log-probability of token v."""
+    T, V = 5, 40
+    hb, wb = _tiny(T, V)
+    rep = np.repeat(hb, V, axis=0)
+    toks = np.tile(np.arange(V), T)
+    lp, H = oracle.logprobs(rep, wb, toks, tau)
+    lp = lp.reshape(T, V)
+    p = np.exp(lp)
+    np.testing.assert_allclose(p.sum(axis=1), 1.0, atol=1e-13)
+    np.testing.assert_allclose(-(p * lp).sum(axis=1), H.reshape(T, V)[:, 0], atol=1e-12)
+    assert (np.ptp(H.reshape(T, V), axis=1) == 0).all()  # entropy does not depend on the token
+
+
+def test_duplicated_vocabulary_shifts_by_log2():
+    hb, wb = _tiny(6, 50)
+    tok = np.array([0, 5, 10, 20, 30, 49])
+    lp, H = oracle.logprobs(hb, wb, tok, 1.0)
+    lp2, H2 = oracle.logprobs(hb, np.concatenate([wb, wb]), tok, 1.0)
+    np.testing.assert_allclose(lp2, lp - math.log(2), atol=1e-12)
+    np.testing.assert_allclose(H2, H + math.log(2), atol=1e-12)
+
+
+def test_vocab_permutation_invariance():
+    hb, wb = _tiny(6, 50)
+    tok = np.array([0, 5, 10, 20, 30, 49])
+    perm = np.random.default_rng(3).permutation(50)
+    inv = np.argsort(perm)
+    lp, H = oracle.logprobs(hb, wb, tok, 1.0)
+    lp2, H2 = oracle.logprobs(hb, wb[perm], inv[tok], 1.0)
+    np.testing.assert_allclose(lp2, lp, atol=1e-12)
+    np.testing.assert_allclose(H2, H, atol=1e-12)
+
+
+def test_temperature_divides_logits():
+    """(2h, tau = 2) equals (h, tau = 1) exactly: doubling is exact in bf16 and fp64.
+    (h, tau) equals the planted logits divided by tau, not multiplied."""
+    hb, wb = _tiny(4, 30)
+    h2 = _bits(oracle.bf16_to_f64(hb) * 2.0)
+    tok = np.array([1, 2, 3, 4])
+    a = oracle.logprobs(hb, wb, tok, 1.0)
+    b = oracle.logprobs(h2, wb, tok, 2.0)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    c = oracle.logprobs(hb, wb, tok, 0.25)
+    assert not np.allclose(a[1], c[1])
+    # tau -> infinity flattens the distribution to uniform
+    _, Hbig = oracle.logprobs(hb, wb, tok, 1e12)
+    np.testing.assert_allclose(Hbig, math.log(30), atol=1e-9)
+
+
+def test_rows_are_independent_and_blocking_is_invisible():
+    hb, wb = _tiny(9, 33)
+    tok = np.arange(9) * 3
+    a = oracle.logprobs(hb, wb, tok, 1.0, row_block=256)
+    b = oracle.logprobs(hb, wb, tok, 1.0, row_block=2)
+    for i in range(9):
+        c = oracle.logprobs(hb[i:i + 1], wb, tok[i:i + 1], 1.0)
+        assert abs(c[0][0] - a[0][i]) <= 1e-14 and abs(c[1][0] - a[1][i]) <= 1e-14
+    np.testing.assert_allclose(a[0], b[0], atol=1e-14)
+    np.testing.assert_allclose(a[1], b[1], atol=1e-14)
+
+
+def test_ranges_on_random_rows():
+    hb, wb = _tiny(20, 500, d=64, scale=3.0)
+    tok = np.random.default_rng(1).integers(0, 500, 20)
+    lp, H = oracle.logprobs(hb, wb, tok, 1.0)
+    assert (lp <= 0).all()
+    assert (H >= 0).all() and (H <= math.log(500) + 1e-12).all()
+
+
+def test_out_of_range_token_gives_nan_logp():
+    hb, wb = _tiny(3, 20)
+    lp, H = oracle.logprobs(hb, wb, np.array([-1, 5, 20]), 1.0)
+    assert np.isnan(lp[0]) and np.isnan(lp[2]) and np.isfinite(lp[1])
+    assert np.isfinite(H).all()
+
+
+# ---------------------------------------------------------------- mismatch
+
+def _table1():
+    rows = np.loadtxt(os.path.join(GOLDEN, "table1_token_logprobs.txt"), comments="#")
+    return rows[:, 1], rows[:, 2], rows[:, 3]
+
+
+def test_mismatch_table1_sign_and_values():
+    """Table 1: delta = log pi_train - log pi_rollout. Each printed value is
+    rounded to 3 decimals, so the recomputed delta is within 1.5e-3."""
+    rollout, train, printed = _table1()
+    delta, k3, w = oracle.mismatch(train, rollout, 2.0)
+    assert np.max(np.abs(delta - printed)) <= 1.5e-3
+    # position 4 is the argmax flip: -0.827 - (-0.694) = -0.133
+    assert abs(delta[3] - (-0.133)) < 1e-12
+    assert abs(k3[3] - 0.0084651) < 5e-7
+    assert abs(w[3] - 0.8754650) < 5e-7
+    # the opposite convention would flip the sign of the large entry
+    d_swapped, _, _ = oracle.mismatch(rollout, train, 2.0)
+    assert abs(d_swapped[3] - printed[3]) > 0.2
+
+
+@pytest.mark.parametrize("C", [0.5, 1.0, 2.0])
+def test_mismatch_identical_inputs(C):
+    x = np.random.default_rng(0).standard_normal(100).astype(np.float32) - 3
+    delta, k3, w = oracle.mismatch(x, x, C)
+    assert (delta == 0).all() and (k3 == 0).all()
+    assert (w == min(1.0, C)).all()
+
+
+def test_k3_literal_form_at_moderate_delta():
+    d = np.array([-3.0, -1.0, -0.5, -0.1, 0.1, 0.5, 1.0, 3.0])
+    _, k3, _ = oracle.mismatch(d, np.zeros_like(d), 2.0)
+    r = np.exp(d)
+    np.testing.assert_allclose(k3, (r - 1) - np.log(r), rtol=1e-12)
+
+
+def test_k3_taylor_series_at_small_delta():
+    d = np.array([-1e-3, -1e-5, -1e-7, 1e-7, 1e-5, 1e-3, 0.001])
+    _, k3, _ = oracle.mismatch(d, np.zeros_like(d), 2.0)
+    series = d ** 2 / 2 + d ** 3 / 6 + d ** 4 / 24 + d ** 5 / 120
+    np.testing.assert_allclose(k3, series, rtol=1e-8)
+    assert abs(k3[-1] - 5.0016670834e-7) < 1e-16
+    assert (oracle.mismatch(np.random.default_rng(1).standard_normal(1000), np.zeros(1000), 2.0)[1] >= 0).all()
+
+
+def test_truncated_weight():
+    d = np.array([math.log(2.0), 0.0, -0.133, 5.0, -50.0])
+    _, _, w = oracle.mismatch(d, np.zeros_like(d), 2.0)
+    assert abs(w[0] - 2.0) < 1e-15
+    assert w[1] == 1.0
+    assert abs(w[2] - math.exp(-0.133)) < 1e-15
+    assert w[3] == 2.0
+    assert 0 < w[4] < 1e-21
+    _, _, wc = oracle.mismatch(np.array([0.0, math.log(0.5) + 1e-9]), np.zeros(2), 0.5)
+    assert wc[0] == 0.5 and wc[1] == 0.5
