@@ -1,0 +1,160 @@
+/*
+ * tim.h -- batch-invariant fused LM-head token log-probabilities and
+ * training-inference mismatch statistics on AMD MI355X (gfx950).
+ *
+ * The quantities follow "Diagnosing Training Inference Mismatch in LLM
+ * Reinforcement Learning" (VeXact):
+ *   - the token log-probability log pi(a_t | s_t) that the rollout engine and
+ *     the trainer must agree on (Section 2; the two sides of Eq. 1), computed
+ *     with kernels whose tiling and reduction order do not depend on how rows
+ *     are batched (the batch-invariance principle of Section 3.1);
+ *   - the per-token discrepancy delta_t of Eq. 1, the K3 estimator of
+ *     Section 4.1 and the truncated importance weight of Eq. 6 (Section 4.2).
+ *
+ * Conventions shared by every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller. The library
+ *     allocates nothing, keeps no state between calls and never synchronises:
+ *     every kernel is enqueued on `stream` (0 = the null stream) and the call
+ *     returns as soon as the launches are enqueued.
+ *   - Argument errors are detected on the host, before anything is enqueued,
+ *     and reported by the return value; on any error no output is written.
+ *   - T == 0 is a successful no-op (pointers are not inspected).
+ *   - A failed kernel launch returns TIM_ERR_HIP; outputs are then undefined.
+ *   - Calls that overlap in time must not share a workspace.
+ */
+#ifndef TIM_H
+#define TIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TIM_OK = 0,
+  TIM_ERR_NULL = 1,      /* a required pointer is NULL */
+  TIM_ERR_SHAPE = 2,     /* T < 0, d not a positive multiple of 128 (256 for TIM_ORDER_SPLITK4),
+                            V outside [1, TIM_MAX_VOCAB] */
+  TIM_ERR_VALUE = 3,     /* temperature or C not finite or <= 0, unknown mode/order,
+                            micro_batch < 0, hidden or w_vocab not 16-byte aligned */
+  TIM_ERR_WORKSPACE = 4, /* workspace NULL or smaller than tim_logprobs_workspace_size() */
+  TIM_ERR_HIP = 5        /* a HIP runtime call or kernel launch failed */
+} tim_status;
+
+/* Launch shape only: both modes compute every row with identical arithmetic,
+ * so their outputs are bitwise equal for any batching of the same rows. */
+typedef enum {
+  TIM_MODE_ROLLOUT = 0,  /* one call per decode step: a ragged batch of rows, one launch */
+  TIM_MODE_TRAINING = 1  /* packed token stream, processed in micro-batches of micro_batch rows */
+} tim_mode;
+
+/* Reduction order. TIM_ORDER_SPLITK4 is a deliberately different order of the
+ * same mathematics (the hidden dimension summed as four separately accumulated
+ * quarters, the vocabulary partials folded left to right instead of by a
+ * balanced tree). It models a second engine whose kernels reduce in another
+ * order -- the second source of mismatch named in Section 3.1 -- and exists to
+ * produce controlled, small mismatches for tim_mismatch. */
+typedef enum {
+  TIM_ORDER_INVARIANT = 0,
+  TIM_ORDER_SPLITK4 = 1
+} tim_order;
+
+/* Vocabulary entries per softmax partial (the fixed vocab tile width). */
+#define TIM_VOCAB_TILE 256
+/* Largest supported vocabulary: 2048 tiles. */
+#define TIM_MAX_VOCAB (2048 * TIM_VOCAB_TILE)
+
+/* Bytes of device workspace tim_logprobs needs for these arguments:
+ * rows_per_launch * ceil(V / TIM_VOCAB_TILE) * 16, where rows_per_launch is T
+ * in rollout mode and min(T, micro_batch) in training mode (micro_batch 0 means
+ * T). Returns 0 for invalid arguments or T == 0. Pure host function. */
+size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch);
+
+/* Token log-probabilities and entropies of T rows (Section 2, Eq. 1's terms).
+ *
+ * For row i, with z_v = (sum_k hidden[i,k] * w_vocab[v,k]) * (1/temperature):
+ *   logp[i]    = z_{tokens[i]} - log sum_v exp(z_v)
+ *   entropy[i] = - sum_v p_v log p_v,  p_v = softmax(z)_v   (nats)
+ *   lse[i]     = log sum_v exp(z_v)
+ *
+ * hidden   bf16 [T, d] row-major, 16-byte aligned (final hidden states).
+ * w_vocab  bf16 [V, d] row-major, 16-byte aligned (LM-head weight, vocab-major).
+ * tokens   int32 [T]; tokens[i] is the token sampled from row i's distribution
+ *          (no label shift is applied). A token outside [0, V) yields
+ *          logp[i] = NaN; entropy[i] and lse[i] are still computed.
+ * temperature  finite and > 0; the logits are multiplied by the fp32 value
+ *          (float)(1.0 / temperature) in every mode and order.
+ * mode, micro_batch  see tim_mode; micro_batch is ignored in rollout mode.
+ * order    tim_order.
+ * logp     fp32 [T] out (required); entropy, lse fp32 [T] out, may be NULL.
+ * workspace, workspace_bytes  device scratch of at least
+ *          tim_logprobs_workspace_size(T, d, V, mode, micro_batch) bytes.
+ *
+ * Arithmetic: bf16 x bf16 products accumulated in fp32 by MFMA with the
+ * hidden dimension in ascending order; fp32 softmax partials per tile of
+ * TIM_VOCAB_TILE vocabulary entries; partials merged by a fixed balanced tree
+ * over the tile index. None of this depends on T, mode, micro_batch or a row's
+ * position in the batch, so with TIM_ORDER_INVARIANT a row's outputs are
+ * bitwise identical however it is batched. NaN or Inf in the inputs
+ * propagates to that row's outputs. */
+tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                        int64_t T, int32_t d, int32_t V, float temperature,
+                        int32_t mode, int64_t micro_batch, int32_t order,
+                        float* logp, float* entropy, float* lse,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* The two stages of tim_logprobs, for callers that schedule them themselves
+ * (a profiler timing one kernel, or a vocabulary-sharded deployment that
+ * exchanges partials between the stages). tim_logprobs over one launch's rows
+ * is exactly tim_logprobs_partials followed by tim_logprobs_merge.
+ *
+ * tim_logprobs_partials: one launch over all T rows (no micro-batching; mode
+ * only picks the row tile). Writes T * ceil(V / TIM_VOCAB_TILE) partials of
+ * 16 bytes (running max, sum of exponentials, sum of exponential-weighted
+ * logit offsets, gathered token logit) into `workspace`, which must hold
+ * tim_logprobs_workspace_size(T, d, V, TIM_MODE_ROLLOUT, 0) bytes. Arguments
+ * and errors as tim_logprobs.
+ *
+ * tim_logprobs_merge: reduces those partials to logp / entropy / lse (same
+ * definitions as tim_logprobs). `tokens`, T, V and `order` must be the ones
+ * given to the partials call; TIM_ORDER_SPLITK4 folds the partials left to
+ * right instead of by the balanced tree. Errors: TIM_ERR_SHAPE for T < 0 or V
+ * out of range, TIM_ERR_NULL for a NULL workspace / tokens / logp,
+ * TIM_ERR_VALUE for an unknown order. */
+tim_status tim_logprobs_partials(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                 int64_t T, int32_t d, int32_t V, float temperature,
+                                 int32_t mode, int32_t order,
+                                 void* workspace, size_t workspace_bytes, hipStream_t stream);
+tim_status tim_logprobs_merge(const void* workspace, const int32_t* tokens, int64_t T, int32_t V,
+                              int32_t order, float* logp, float* entropy, float* lse,
+                              hipStream_t stream);
+
+/* Token-level mismatch statistics between two evaluations of the same tokens
+ * (Section 2, Eq. 1; Section 4.1 K3; Section 4.2 r_corr and Eq. 6):
+ *   log_ratio[i] = logp_a[i] - logp_b[i]          (delta_t; a = trainer, b = rollout)
+ *   k3[i]        = expm1(delta) - delta            ((r - 1) - log r with r = exp(delta))
+ *   is_weight[i] = min(exp(delta), C)              (truncated correction ratio)
+ * All fp32 device arrays of length T; any output may be NULL (not written).
+ * C must be finite and > 0 (the paper's tau_tok is 2). */
+tim_status tim_mismatch(const float* logp_a, const float* logp_b, int64_t T, float C,
+                        float* log_ratio, float* k3, float* is_weight, hipStream_t stream);
+
+/* Test and debugging aid: writes the fp32 logits z[T, V] (row-major) exactly as
+ * tim_logprobs forms them before the softmax (same kernel code, same
+ * accumulation order, same temperature multiply), for checking the gather and
+ * the contraction element by element. Same argument rules as tim_logprobs;
+ * `order` selects the accumulation order. */
+tim_status tim_logits(const void* hidden, const void* w_vocab, int64_t T, int32_t d, int32_t V,
+                      float temperature, int32_t order, float* logits, hipStream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char* tim_status_string(tim_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TIM_H */

@@ -1,0 +1,208 @@
+"""Python binding of libtim.so: batch-invariant fused LM-head token log-probs
+and training-inference mismatch statistics on MI355X (gfx950).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C ABI (include/tim.h). Tensors must live on the GPU; the
+calls are enqueued on torch's current stream. There is no fallback: when the
+library is missing or no GPU is present the calls raise.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import enum
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtim.so")
+
+VOCAB_TILE = 256
+MAX_VOCAB = 2048 * VOCAB_TILE
+
+
+class Status(enum.IntEnum):
+    OK = 0
+    ERR_NULL = 1
+    ERR_SHAPE = 2
+    ERR_VALUE = 3
+    ERR_WORKSPACE = 4
+    ERR_HIP = 5
+
+
+class Mode(enum.IntEnum):
+    ROLLOUT = 0
+    TRAINING = 1
+
+
+class Order(enum.IntEnum):
+    INVARIANT = 0
+    SPLITK4 = 1
+
+
+class TimError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = Status(status)
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libtim.so and declare its C signatures. Raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError(f"{path} is not built; run `python -m paper_2605_14220_amd.build`")
+    lib = ctypes.CDLL(path)
+    c = ctypes
+    lib.tim_logprobs_workspace_size.restype = c.c_size_t
+    lib.tim_logprobs_workspace_size.argtypes = [c.c_int64, c.c_int32, c.c_int32, c.c_int32, c.c_int64]
+    lib.tim_logprobs.restype = c.c_int
+    lib.tim_logprobs.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
+                                 c.c_float, c.c_int32, c.c_int64, c.c_int32, c.c_void_p, c.c_void_p,
+                                 c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p]
+    lib.tim_logprobs_partials.restype = c.c_int
+    lib.tim_logprobs_partials.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32,
+                                          c.c_int32, c.c_float, c.c_int32, c.c_int32, c.c_void_p,
+                                          c.c_size_t, c.c_void_p]
+    lib.tim_logprobs_merge.restype = c.c_int
+    lib.tim_logprobs_merge.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
+                                       c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p]
+    lib.tim_mismatch.restype = c.c_int
+    lib.tim_mismatch.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_float, c.c_void_p, c.c_void_p,
+                                 c.c_void_p, c.c_void_p]
+    lib.tim_logits.restype = c.c_int
+    lib.tim_logits.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32, c.c_float,
+                               c.c_int32, c.c_void_p, c.c_void_p]
+    lib.tim_status_string.restype = c.c_char_p
+    lib.tim_status_string.argtypes = [c.c_int]
+    _lib = lib
+    return lib
+
+
+def _check(status: int):
+    if status != 0:
+        msg = load_library().tim_status_string(status).decode()
+        raise TimError(status, msg)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _require_gpu(*tensors):
+    for t in tensors:
+        if t is not None and not t.is_cuda:
+            raise ValueError("tim: tensors must be on the GPU")
+        if t is not None and not t.is_contiguous():
+            raise ValueError("tim: tensors must be contiguous")
+
+
+def workspace_size(T: int, d: int, V: int, mode: Mode = Mode.TRAINING, micro_batch: int = 0) -> int:
+    """Bytes of workspace tim_logprobs needs (0 for T == 0 or invalid shapes)."""
+    return int(load_library().tim_logprobs_workspace_size(int(T), int(d), int(V), int(mode), int(micro_batch)))
+
+
+def logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor, temperature: float = 1.0,
+             mode: Mode = Mode.TRAINING, micro_batch: int = 0, order: Order = Order.INVARIANT,
+             entropy: bool = True, lse: bool = False, workspace: torch.Tensor | None = None,
+             out: tuple | None = None):
+    """Token log-probabilities (and entropies, log-normalisers) of T rows.
+
+    hidden bf16 [T, d], w_vocab bf16 [V, d], tokens int32 [T], all on one GPU.
+    Returns (logp, entropy or None, lse or None), fp32 [T] each."""
+    lib = load_library()
+    if hidden.dtype != torch.bfloat16 or w_vocab.dtype != torch.bfloat16:
+        raise TypeError("tim.logprobs: hidden and w_vocab must be bfloat16")
+    if tokens.dtype != torch.int32:
+        raise TypeError("tim.logprobs: tokens must be int32")
+    if hidden.dim() != 2 or w_vocab.dim() != 2 or hidden.shape[1] != w_vocab.shape[1]:
+        raise ValueError("tim.logprobs: hidden [T, d] and w_vocab [V, d] must share d")
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    if tokens.shape != (T,):
+        raise ValueError("tim.logprobs: tokens must be [T]")
+    _require_gpu(hidden, w_vocab, tokens, workspace)
+    dev = hidden.device
+    if out is None:
+        lp = torch.empty(T, dtype=torch.float32, device=dev)
+        ent = torch.empty(T, dtype=torch.float32, device=dev) if entropy else None
+        ls = torch.empty(T, dtype=torch.float32, device=dev) if lse else None
+    else:
+        lp, ent, ls = out
+        _require_gpu(lp, ent, ls)
+    if T == 0:
+        return lp, ent, ls
+    need = workspace_size(T, d, V, mode, micro_batch)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.tim_logprobs(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature),
+                            int(mode), int(micro_batch), int(order), _ptr(lp), _ptr(ent), _ptr(ls),
+                            _ptr(workspace), ws_bytes, _stream(dev)))
+    return lp, ent, ls
+
+
+def logprobs_partials(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor,
+                      workspace: torch.Tensor, temperature: float = 1.0, mode: Mode = Mode.TRAINING,
+                      order: Order = Order.INVARIANT):
+    """First stage of logprobs over all rows in one launch: per-(row, vocab tile)
+    partials written into `workspace` (see include/tim.h)."""
+    lib = load_library()
+    _require_gpu(hidden, w_vocab, tokens, workspace)
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.tim_logprobs_partials(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature),
+                                     int(mode), int(order), _ptr(workspace), ws_bytes, _stream(hidden.device)))
+
+
+def logprobs_merge(workspace: torch.Tensor, tokens: torch.Tensor, V: int, order: Order = Order.INVARIANT,
+                   out: tuple | None = None):
+    """Second stage: partials in `workspace` -> (logp, entropy, lse) for len(tokens) rows."""
+    lib = load_library()
+    _require_gpu(workspace, tokens)
+    T = tokens.numel()
+    if out is None:
+        out = tuple(torch.empty(T, dtype=torch.float32, device=tokens.device) for _ in range(3))
+    _require_gpu(*out)
+    _check(lib.tim_logprobs_merge(_ptr(workspace), _ptr(tokens), T, int(V), int(order), _ptr(out[0]),
+                                  _ptr(out[1]), _ptr(out[2]), _stream(tokens.device)))
+    return out
+
+
+def mismatch(logp_a: torch.Tensor, logp_b: torch.Tensor, C: float = 2.0, out: tuple | None = None):
+    """(log_ratio, k3, is_weight) fp32 [T]: delta = a - b, k3 = expm1(delta) - delta,
+    w = min(exp(delta), C). a is the trainer's log-prob, b the rollout engine's."""
+    lib = load_library()
+    if logp_a.dtype != torch.float32 or logp_b.dtype != torch.float32 or logp_a.shape != logp_b.shape:
+        raise TypeError("tim.mismatch: logp_a and logp_b must be fp32 of one shape")
+    _require_gpu(logp_a, logp_b)
+    T = logp_a.numel()
+    if out is None:
+        out = tuple(torch.empty_like(logp_a) for _ in range(3))
+    _require_gpu(*out)
+    _check(lib.tim_mismatch(_ptr(logp_a), _ptr(logp_b), T, float(C), _ptr(out[0]), _ptr(out[1]),
+                            _ptr(out[2]), _stream(logp_a.device)))
+    return out
+
+
+def logits(hidden: torch.Tensor, w_vocab: torch.Tensor, temperature: float = 1.0,
+           order: Order = Order.INVARIANT) -> torch.Tensor:
+    """fp32 [T, V] logits exactly as tim_logprobs forms them (test/debug aid)."""
+    lib = load_library()
+    _require_gpu(hidden, w_vocab)
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    z = torch.empty((T, V), dtype=torch.float32, device=hidden.device)
+    _check(lib.tim_logits(_ptr(hidden), _ptr(w_vocab), T, d, V, float(temperature), int(order), _ptr(z),
+                          _stream(hidden.device)))
+    return z

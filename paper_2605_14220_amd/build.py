@@ -1,0 +1,72 @@
+"""Build libtim.so (the C-ABI library) for gfx950 with hipcc, in-tree.
+
+    python -m paper_2605_14220_amd.build            # build
+    python -m paper_2605_14220_amd.build --asm DIR  # also keep the device assembly in DIR
+"""
+
+from __future__ import annotations
+
+import argparse
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+LIB = os.path.join(PKG, "libtim.so")
+SOURCES = ["lmhead.hip", "mismatch.hip", "tim_api.hip"]
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+FLAGS = [
+    f"--offload-arch={ARCH}",
+    "-O3",
+    "-std=c++17",
+    "-fPIC",
+    "-shared",
+    # Every floating-point operation is written out explicitly (fmaf where a
+    # fused multiply-add is meant); the compiler may not contract a * b + c.
+    "-ffp-contract=off",
+    # Keep the compiler from forming packed fp32 arithmetic.
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall",
+    "-Wno-unused-function",
+]
+
+
+def build(asm_dir: str | None = None, verbose: bool = False) -> str:
+    if shutil.which(HIPCC) is None and not os.path.exists(HIPCC):
+        raise RuntimeError(f"hipcc not found at {HIPCC}")
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+    cwd = None
+    if asm_dir:
+        os.makedirs(asm_dir, exist_ok=True)
+        cmd.insert(1, "-save-temps")
+        cwd = asm_dir
+    if verbose:
+        print(" ".join(cmd))
+    r = subprocess.run(cmd, cwd=cwd, capture_output=True, text=True)
+    out = "\n".join(line for line in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in line)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{out}")
+    if verbose and out.strip():
+        print(out)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--asm", default=None, help="directory for -save-temps output")
+    ap.add_argument("-v", "--verbose", action="store_true")
+    args = ap.parse_args(argv)
+    print(build(args.asm, args.verbose))
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,149 @@
+// C-ABI entry points: argument checks, launch planning, launches.
+//
+// The planner only chooses launch shapes. Rollout mode sends the whole ragged
+// batch in one launch with a row tile sized to the batch (64, 128 or 256 rows
+// per workgroup); training mode walks the packed stream in micro-batches with
+// 256-row tiles. Every shape runs the same per-row instruction sequence.
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+#include "tim.h"
+#include "validate.h"
+
+namespace {
+
+inline tim_status hip_status(hipError_t e) { return e == hipSuccess ? TIM_OK : TIM_ERR_HIP; }
+
+inline float inv_temperature(float temperature) {
+  return (float)(1.0 / (double)temperature);
+}
+
+// Row tile (in 32-row blocks per wave) for a launch of `rows` rows.
+inline int token_blocks_for(int64_t rows, int32_t mode, bool splitk4) {
+  int tb = 4;
+  if (mode == TIM_MODE_ROLLOUT) tb = rows <= 64 ? 1 : (rows <= 128 ? 2 : 4);
+  if (splitk4 && tb > 2) tb = 2;  // the split-K engine keeps a second accumulator set
+  return tb;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch) {
+  if (T <= 0 || tim::check_shape(T, d, V, TIM_ORDER_INVARIANT) != TIM_OK) return 0;
+  if (!tim::valid_mode(mode) || micro_batch < 0) return 0;
+  return tim::workspace_bytes(T, V, mode, micro_batch);
+}
+
+tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,
+                        int32_t d, int32_t V, float temperature, int32_t mode, int64_t micro_batch,
+                        int32_t order, float* logp, float* entropy, float* lse, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  tim_status st = tim::validate_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode,
+                                         micro_batch, order, logp, workspace, workspace_bytes);
+  if (st != TIM_OK || T == 0) return st;
+
+  const bool splitk4 = order == TIM_ORDER_SPLITK4;
+  const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
+  const int tb = token_blocks_for(step, mode, splitk4);
+  const float inv_tau = inv_temperature(temperature);
+  const __bf16* h = (const __bf16*)hidden;
+  tim::Partial* part = (tim::Partial*)workspace;
+
+  for (int64_t t0 = 0; t0 < T; t0 += step) {
+    const int64_t rows = (T - t0) < step ? (T - t0) : step;
+    tim::LmHeadArgs a;
+    a.hidden = h + t0 * d;
+    a.w = w_vocab;
+    a.tokens = tokens + t0;
+    a.rows = rows;
+    a.d = d;
+    a.V = V;
+    a.inv_tau = inv_tau;
+    a.part = part;
+    a.logits = nullptr;
+    st = hip_status(tim::launch_partials(a, tb, splitk4, stream));
+    if (st != TIM_OK) return st;
+    st = hip_status(tim::launch_merge(part, tokens + t0, rows, V, splitk4, logp + t0,
+                                      entropy ? entropy + t0 : nullptr, lse ? lse + t0 : nullptr,
+                                      stream));
+    if (st != TIM_OK) return st;
+  }
+  return TIM_OK;
+}
+
+tim_status tim_logprobs_partials(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                 int64_t T, int32_t d, int32_t V, float temperature, int32_t mode,
+                                 int32_t order, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
+  const tim_status st = tim::validate_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode, 0,
+                                               order, /*logp=*/(const float*)workspace, workspace,
+                                               workspace_bytes);
+  if (st != TIM_OK || T == 0) return st;
+  const bool splitk4 = order == TIM_ORDER_SPLITK4;
+  tim::LmHeadArgs a;
+  a.hidden = hidden;
+  a.w = w_vocab;
+  a.tokens = tokens;
+  a.rows = T;
+  a.d = d;
+  a.V = V;
+  a.inv_tau = inv_temperature(temperature);
+  a.part = (tim::Partial*)workspace;
+  a.logits = nullptr;
+  return hip_status(tim::launch_partials(a, token_blocks_for(T, mode, splitk4), splitk4, stream));
+}
+
+tim_status tim_logprobs_merge(const void* workspace, const int32_t* tokens, int64_t T, int32_t V,
+                              int32_t order, float* logp, float* entropy, float* lse,
+                              hipStream_t stream) {
+  if (T < 0) return TIM_ERR_SHAPE;
+  if (T == 0) return TIM_OK;
+  if (!workspace || !tokens || !logp) return TIM_ERR_NULL;
+  if (V < 1 || V > TIM_MAX_VOCAB) return TIM_ERR_SHAPE;
+  if (!tim::valid_order(order)) return TIM_ERR_VALUE;
+  return hip_status(tim::launch_merge((const tim::Partial*)workspace, tokens, T, V,
+                                      order == TIM_ORDER_SPLITK4, logp, entropy, lse, stream));
+}
+
+tim_status tim_mismatch(const float* logp_a, const float* logp_b, int64_t T, float C,
+                        float* log_ratio, float* k3, float* is_weight, hipStream_t stream) {
+  const tim_status st = tim::validate_mismatch(logp_a, logp_b, T, C);
+  if (st != TIM_OK || T == 0) return st;
+  if (!log_ratio && !k3 && !is_weight) return TIM_OK;
+  return hip_status(tim::launch_mismatch(logp_a, logp_b, T, C, log_ratio, k3, is_weight, stream));
+}
+
+tim_status tim_logits(const void* hidden, const void* w_vocab, int64_t T, int32_t d, int32_t V,
+                      float temperature, int32_t order, float* logits, hipStream_t stream) {
+  const tim_status st = tim::validate_logits(hidden, w_vocab, T, d, V, temperature, order, logits);
+  if (st != TIM_OK || T == 0) return st;
+  const bool splitk4 = order == TIM_ORDER_SPLITK4;
+  tim::LmHeadArgs a;
+  a.hidden = hidden;
+  a.w = w_vocab;
+  a.tokens = nullptr;
+  a.rows = T;
+  a.d = d;
+  a.V = V;
+  a.inv_tau = inv_temperature(temperature);
+  a.part = nullptr;
+  a.logits = logits;
+  return hip_status(tim::launch_partials(a, splitk4 ? 2 : 4, splitk4, stream));
+}
+
+const char* tim_status_string(tim_status s) {
+  switch (s) {
+    case TIM_OK: return "TIM_OK";
+    case TIM_ERR_NULL: return "TIM_ERR_NULL: a required pointer is NULL";
+    case TIM_ERR_SHAPE: return "TIM_ERR_SHAPE: T, d or V out of range";
+    case TIM_ERR_VALUE: return "TIM_ERR_VALUE: bad temperature, C, mode, order, micro_batch or alignment";
+    case TIM_ERR_WORKSPACE: return "TIM_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case TIM_ERR_HIP: return "TIM_ERR_HIP: a HIP call or kernel launch failed";
+  }
+  return "unknown tim_status";
+}
+
+}  // extern "C"

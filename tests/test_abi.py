@@ -1,0 +1,215 @@
+"""The C-ABI library on the host: it loads, exports every entry point that
+include/tim.h declares, sizes workspaces by the documented formula and rejects
+every bad argument with the documented status before touching the GPU.
+
+No call here reaches a kernel launch: each passes an argument that the host
+checks reject (or T == 0), so these tests run without a GPU.
+"""
+
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2605_14220_amd as tim
+from paper_2605_14220_amd import Mode, Order, Status
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tim.h")
+
+FAKE = 0x10000        # 16-byte aligned, never dereferenced (rejected before any launch)
+FAKE_MIS = 0x10008    # misaligned
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[\w\s\*]+?\b(tim_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return tim.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    assert names == ["tim_logits", "tim_logprobs", "tim_logprobs_merge", "tim_logprobs_partials",
+                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_status_string"]
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", tim.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT\s+(\w+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for s in Status:
+        text = lib.tim_status_string(int(s)).decode()
+        assert text.startswith("TIM_OK" if s == 0 else "TIM_ERR_")
+    assert lib.tim_status_string(99).decode() == "unknown tim_status"
+
+
+@pytest.mark.parametrize("T,d,V,mode,mb", [
+    (64, 256, 4096, Mode.TRAINING, 0),
+    (147000, 4096, 151936, Mode.TRAINING, 16384),
+    (147000, 4096, 151936, Mode.TRAINING, 200000),
+    (200, 4096, 151936, Mode.ROLLOUT, 16384),
+    (5, 128, 1, Mode.ROLLOUT, 0),
+    (131072, 5120, 152064, Mode.TRAINING, 32768),
+])
+def test_workspace_size_formula(lib, T, d, V, mode, mb):
+    rows = T if (mode == Mode.ROLLOUT or mb == 0 or mb >= T) else mb
+    assert tim.workspace_size(T, d, V, mode, mb) == rows * math.ceil(V / 256) * 16
+
+
+@pytest.mark.parametrize("args", [(0, 256, 4096, 1, 0), (-1, 256, 4096, 1, 0), (10, 100, 4096, 1, 0),
+                                  (10, 256, 0, 1, 0), (10, 256, 4096, 7, 0), (10, 256, 4096, 1, -1),
+                                  (10, 256, 2048 * 256 + 1, 1, 0)])
+def test_workspace_size_zero_when_invalid(lib, args):
+    assert lib.tim_logprobs_workspace_size(*args) == 0
+
+
+def _lp(lib, hidden=FAKE, w=FAKE, tokens=FAKE, T=8, d=256, V=4096, tau=1.0, mode=1, mb=0, order=0,
+        logp=FAKE, ent=None, lse=None, ws=FAKE, ws_bytes=None):
+    if ws_bytes is None:
+        ws_bytes = 1 << 40
+    return lib.tim_logprobs(hidden, w, tokens, T, d, V, tau, mode, mb, order, logp, ent, lse, ws, ws_bytes, None)
+
+
+def test_logprobs_T_zero_is_noop_even_with_null_pointers(lib):
+    assert _lp(lib, hidden=None, w=None, tokens=None, logp=None, ws=None, T=0) == Status.OK
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(hidden=None), Status.ERR_NULL),
+    (dict(w=None), Status.ERR_NULL),
+    (dict(tokens=None), Status.ERR_NULL),
+    (dict(logp=None), Status.ERR_NULL),
+    (dict(d=0), Status.ERR_SHAPE),
+    (dict(d=-128), Status.ERR_SHAPE),
+    (dict(d=64), Status.ERR_SHAPE),
+    (dict(d=200), Status.ERR_SHAPE),
+    (dict(d=384, order=1), Status.ERR_SHAPE),
+    (dict(V=0), Status.ERR_SHAPE),
+    (dict(V=-5), Status.ERR_SHAPE),
+    (dict(V=2048 * 256 + 1), Status.ERR_SHAPE),
+    (dict(tau=0.0), Status.ERR_VALUE),
+    (dict(tau=-1.0), Status.ERR_VALUE),
+    (dict(tau=float("nan")), Status.ERR_VALUE),
+    (dict(tau=float("inf")), Status.ERR_VALUE),
+    (dict(mode=2), Status.ERR_VALUE),
+    (dict(mode=-1), Status.ERR_VALUE),
+    (dict(order=2), Status.ERR_VALUE),
+    (dict(mb=-1), Status.ERR_VALUE),
+    (dict(hidden=FAKE_MIS), Status.ERR_VALUE),
+    (dict(w=FAKE_MIS), Status.ERR_VALUE),
+    (dict(ws=None), Status.ERR_WORKSPACE),
+    (dict(ws=FAKE_MIS), Status.ERR_WORKSPACE),
+    (dict(ws_bytes=8 * 16 * 16 - 1), Status.ERR_WORKSPACE),
+    (dict(ws_bytes=0), Status.ERR_WORKSPACE),
+    (dict(T=100, mb=10, ws_bytes=10 * 16 * 16 - 16), Status.ERR_WORKSPACE),
+])
+def test_logprobs_rejects(lib, kw, expect):
+    assert _lp(lib, **kw) == expect
+
+
+def test_logprobs_error_precedence(lib):
+    # shape errors are reported before value errors, value before workspace
+    assert _lp(lib, d=100, tau=-1.0, ws=None) == Status.ERR_SHAPE
+    assert _lp(lib, tau=-1.0, ws=None) == Status.ERR_VALUE
+    assert _lp(lib, hidden=None, d=100) == Status.ERR_NULL
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-3), Status.ERR_SHAPE),
+    (dict(a=None), Status.ERR_NULL),
+    (dict(b=None), Status.ERR_NULL),
+    (dict(C=0.0), Status.ERR_VALUE),
+    (dict(C=-2.0), Status.ERR_VALUE),
+    (dict(C=float("nan")), Status.ERR_VALUE),
+    (dict(C=float("inf")), Status.ERR_VALUE),
+])
+def test_mismatch_rejects(lib, kw, expect):
+    a = kw.get("a", FAKE)
+    b = kw.get("b", FAKE)
+    assert lib.tim_mismatch(a, b, kw.get("T", 8), kw.get("C", 2.0), FAKE, FAKE, FAKE, None) == expect
+
+
+def test_mismatch_noops(lib):
+    assert lib.tim_mismatch(None, None, 0, 2.0, None, None, None, None) == Status.OK
+    # every output NULL: nothing to compute, nothing launched
+    assert lib.tim_mismatch(FAKE, FAKE, 8, 2.0, None, None, None, None) == Status.OK
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(out=None), Status.ERR_NULL),
+    (dict(hidden=None), Status.ERR_NULL),
+    (dict(d=96), Status.ERR_SHAPE),
+    (dict(V=0), Status.ERR_SHAPE),
+    (dict(tau=0.0), Status.ERR_VALUE),
+    (dict(order=3), Status.ERR_VALUE),
+    (dict(hidden=FAKE_MIS), Status.ERR_VALUE),
+])
+def test_logits_rejects(lib, kw, expect):
+    args = dict(hidden=FAKE, w=FAKE, T=4, d=256, V=300, tau=1.0, order=0, out=FAKE)
+    args.update(kw)
+    assert lib.tim_logits(args["hidden"], args["w"], args["T"], args["d"], args["V"], args["tau"],
+                          args["order"], args["out"], None) == expect
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(ws=None), Status.ERR_NULL),
+    (dict(tokens=None), Status.ERR_NULL),
+    (dict(logp=None), Status.ERR_NULL),
+    (dict(V=0), Status.ERR_SHAPE),
+    (dict(order=9), Status.ERR_VALUE),
+])
+def test_merge_rejects(lib, kw, expect):
+    a = dict(ws=FAKE, tokens=FAKE, T=4, V=300, order=0, logp=FAKE)
+    a.update(kw)
+    assert lib.tim_logprobs_merge(a["ws"], a["tokens"], a["T"], a["V"], a["order"], a["logp"], None, None,
+                                  None) == expect
+    assert lib.tim_logprobs_merge(None, None, 0, 300, 0, None, None, None, None) == Status.OK
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(hidden=None), Status.ERR_NULL),
+    (dict(ws=None), Status.ERR_NULL),
+    (dict(d=100), Status.ERR_SHAPE),
+    (dict(tau=0.0), Status.ERR_VALUE),
+    (dict(mode=5), Status.ERR_VALUE),
+    (dict(ws_bytes=4 * 2 * 16 - 1), Status.ERR_WORKSPACE),
+])
+def test_partials_rejects(lib, kw, expect):
+    a = dict(hidden=FAKE, w=FAKE, tokens=FAKE, T=4, d=256, V=300, tau=1.0, mode=1, order=0, ws=FAKE,
+             ws_bytes=1 << 30)
+    a.update(kw)
+    assert lib.tim_logprobs_partials(a["hidden"], a["w"], a["tokens"], a["T"], a["d"], a["V"], a["tau"],
+                                     a["mode"], a["order"], a["ws"], a["ws_bytes"], None) == expect
+
+
+def test_python_binding_rejects_cpu_tensors():
+    import torch
+    h = torch.zeros(4, 256, dtype=torch.bfloat16)
+    w = torch.zeros(300, 256, dtype=torch.bfloat16)
+    tok = torch.zeros(4, dtype=torch.int32)
+    with pytest.raises(ValueError, match="GPU"):
+        tim.logprobs(h, w, tok)
+    with pytest.raises(TypeError):
+        tim.logprobs(h.float(), w, tok)
+    with pytest.raises(TypeError):
+        tim.logprobs(h, w, tok.long())
+    with pytest.raises(ValueError, match="GPU"):
+        tim.mismatch(torch.zeros(3), torch.zeros(3))

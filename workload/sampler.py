@@ -27,13 +27,14 @@ def sample_tokens(h: torch.Tensor, W: torch.Tensor, temperature: float, u: np.nd
     dev = h.device
     out = torch.empty(T, dtype=torch.int32, device=dev)
     u_t = torch.as_tensor(np.asarray(u, dtype=np.float64), device=dev)
+    Wd = W.to(dtype)
     for r0 in range(0, T, row_chunk):
         r1 = min(T, r0 + row_chunk)
         hb = h[r0:r1].to(dtype)
         z = torch.empty((r1 - r0, V), dtype=dtype, device=dev)
         for v0 in range(0, V, vocab_chunk):
             v1 = min(V, v0 + vocab_chunk)
-            z[:, v0:v1] = torch.nn.functional.linear(hb, W[v0:v1].to(dtype))
+            z[:, v0:v1] = torch.nn.functional.linear(hb, Wd[v0:v1])
         z /= temperature
         z -= z.max(dim=1, keepdim=True).values
         p = torch.exp(z)
