@@ -92,6 +92,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="mid")
     ap.add_argument("--cpu-rows", type=int, default=2048, help="rows of the oracle CPU baseline (0 = skip)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after timing, run a plain copy kernel of known size (torch.neg over 2^28 fp32: "
+                         "1 GiB read + 1 GiB written) so a counter profile can scale HBM byte counters")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path runs on a single GPU, "
@@ -189,6 +192,15 @@ def main(argv=None):
     log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step ({wall / args.steps * 1e3:.3f} wall), "
         f"{tok_per_s:,.0f} tokens/s, path {path_tflops:.1f} TFLOP/s = {path_tflops / PEAK_BF16_TFLOPS:.1%} of "
         f"bf16 peak; partials kernel {avg_ms:.3f} ms/launch = {achieved_tflops:.1f} TFLOP/s")
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("[bench] calibration copy: 3 x torch.neg over 2^28 fp32 (1 GiB in, 1 GiB out)")
 
     # mismatch report between the two engines (context)
     dl = stats[0].abs()

@@ -38,11 +38,14 @@ FLAGS = [
 ]
 
 
-def build(asm_dir: str | None = None, verbose: bool = False) -> str:
+def build(asm_dir: str | None = None, verbose: bool = False, defines=(), out: str = LIB) -> str:
+    """Compile the library. `defines` are NAME=VALUE pipeline-shape overrides
+    (TIM_KSTAGE, TIM_NBUF, TIM_SWZ_SHIFT, TIM_GROUP_V); they never change results."""
     if shutil.which(HIPCC) is None and not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+    tmp = out + ".tmp"
+    cmd = [HIPCC, *FLAGS, *[f"-D{x}" for x in defines], "-I", INCLUDE, "-I", CSRC,
+           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
     cwd = None
     if asm_dir:
         os.makedirs(asm_dir, exist_ok=True)
@@ -51,21 +54,23 @@ def build(asm_dir: str | None = None, verbose: bool = False) -> str:
     if verbose:
         print(" ".join(cmd))
     r = subprocess.run(cmd, cwd=cwd, capture_output=True, text=True)
-    out = "\n".join(line for line in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in line)
+    log = "\n".join(line for line in (r.stdout + r.stderr).splitlines() if "packed-fp32-ops" not in line)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{out}")
-    if verbose and out.strip():
-        print(out)
-    os.replace(tmp, LIB)
-    return LIB
+        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{log}")
+    if verbose and log.strip():
+        print(log)
+    os.replace(tmp, out)
+    return out
 
 
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--asm", default=None, help="directory for -save-temps output")
     ap.add_argument("-v", "--verbose", action="store_true")
+    ap.add_argument("-D", dest="defines", action="append", default=[], help="NAME=VALUE pipeline override")
+    ap.add_argument("-o", dest="out", default=LIB)
     args = ap.parse_args(argv)
-    print(build(args.asm, args.verbose))
+    print(build(args.asm, args.verbose, args.defines, args.out))
 
 
 if __name__ == "__main__":

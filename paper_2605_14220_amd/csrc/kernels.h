@@ -8,7 +8,6 @@
 namespace tim {
 
 constexpr int kVocabTile = 256;   // vocabulary entries per softmax partial
-constexpr int kKStage = 64;       // hidden-dimension elements per LDS stage
 constexpr int kMaxTiles = 2048;   // merge supports up to 64 lanes x 32 leaves
 
 // One partial per (row, vocab tile): running max, sum of exp(z - m),
@@ -32,9 +31,9 @@ struct LmHeadArgs {
 
 int n_vocab_tiles(int V);
 
-// Partials of every (row, vocab tile). token_blocks in {1, 2, 4} selects the
-// rows per workgroup (64, 128, 256); it changes the launch shape only.
-hipError_t launch_partials(const LmHeadArgs& a, int token_blocks, bool splitk4, hipStream_t s);
+// Partials of every (row, vocab tile). rows_per_wg in {64, 128, 256} is the
+// row tile of one workgroup; it changes the launch shape only.
+hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, hipStream_t s);
 // Fixed-order merge of each row's partials into logp / entropy / lse.
 hipError_t launch_merge(const Partial* part, const int32_t* tokens, int64_t rows, int V,
                         bool left_fold, float* logp, float* entropy, float* lse, hipStream_t s);

@@ -47,38 +47,108 @@ struct rsrc_t {
 };
 #endif
 
-constexpr int kRowBytes = kKStage * 2;   // bytes of one row in one stage (128)
+// Compile-time pipeline shape. None of these changes the arithmetic: the
+// hidden dimension is accumulated in the same ascending 16-element MFMA steps
+// whatever the stage depth, buffer count, LDS swizzle or tile order.
+#ifndef TIM_KSTAGE
+#define TIM_KSTAGE 64      // hidden-dimension elements per LDS stage (32 or 64)
+#endif
+#ifndef TIM_NBUF
+#define TIM_NBUF 2         // LDS stage buffers (>= 2)
+#endif
+#ifndef TIM_SWZ_SHIFT     // LDS XOR swizzle: chunk ^= (row >> shift) & (chunks - 1); these
+#if TIM_KSTAGE == 64       // shifts make the 16 lanes of each ds_read_b128 phase hit 16
+#define TIM_SWZ_SHIFT 1    // distinct 16-byte bank groups of the 64 banks
+#else
+#define TIM_SWZ_SHIFT 2
+#endif
+#endif
+#ifndef TIM_GROUP_V
+#define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
+#endif
+#ifndef TIM_TRAIN_ROWS
+#define TIM_TRAIN_ROWS 256 // row tile of full-size launches: 256 (one workgroup per CU) or 128 (two)
+#endif
+#ifndef TIM_WIDE_WAVES
+#define TIM_WIDE_WAVES 1   // 256-row tiles: 8 waves of 128x64 (2 per SIMD); 0 = 4 waves of 128x128
+#endif
+
+constexpr int kKS = TIM_KSTAGE;
+constexpr int kRowBytes = kKS * 2;       // bytes of one row in one stage
+constexpr int kChunks = kRowBytes / 16;  // 16-byte chunks per row per stage
+constexpr int kSteps = kKS / 16;         // MFMA k-steps per stage
 constexpr int kWBytes = kVocabTile * kRowBytes;
+static_assert(kKS == 32 || kKS == 64, "stage depth");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
-template <int NTB>
+// Workgroup shape: 2 waves along the vocab tile (128 entries each) times WT
+// waves along the rows, each wave holding NTB blocks of 32 rows.
+template <int NTB, int WT>
 struct Tile {
-  static constexpr int BT = 2 * NTB * 32;               // rows per workgroup
+  static constexpr int NW = 2 * WT;            // waves per workgroup
+  static constexpr int BT = WT * NTB * 32;     // rows per workgroup
   static constexpr int kHBytes = BT * kRowBytes;
   static constexpr int kStageBytes = kWBytes + kHBytes;
 };
 
-// 16-byte chunk c of row r sits at physical chunk c ^ swz(r) of that row.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+// Residency and pipeline depth of one kernel shape. Shapes whose wave holds
+// at most 128 x 64 accumulators (and no second accumulator set) are built to
+// run two workgroups per CU -- two waves per SIMD from independent
+// workgroups, so one workgroup's barrier stalls and epilogue overlap the
+// other's MFMA stream -- and then get as many LDS stage buffers as fit in
+// half of the 160 KB LDS.
+template <int NTB, int WT, bool SPLITK4>
+struct Shape {
+  using TL = Tile<NTB, WT>;
+  static constexpr int PER_CU =
+      (WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1;
+  static constexpr int FIT = (160 * 1024 / PER_CU) / TL::kStageBytes;
+  static constexpr int NBUF = FIT < TIM_NBUF ? FIT : TIM_NBUF;
+  static_assert(NBUF >= 2, "double buffering at least");
+};
 
+// 16-byte chunk c of row r sits at physical chunk c ^ swz(r) of that row.
+__device__ __forceinline__ int swz(int r) { return (r >> TIM_SWZ_SHIFT) & (kChunks - 1); }
+
+// s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their maxima): at most N of
+// this wave's vector-memory loads (here: global->LDS DMA) are still in flight.
+template <int N>
 __device__ __forceinline__ void wait_vmem() {
-  // s_waitcnt vmcnt(0): every outstanding global->LDS load of this wave landed.
-  __builtin_amdgcn_s_waitcnt(0x0F70);
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+// s_waitcnt vmcnt(N) lgkmcnt(0): additionally every LDS access of this wave done.
+template <int N>
+__device__ __forceinline__ void wait_lgkm0_vmem() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
 }
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Workgroup barrier between pipeline stages. Each wave has already waited
+// for what the barrier must order (its own DMA of the next stage, and its own
+// reads of the buffer about to be refilled), so no memory fence is needed;
+// the empty asm statements keep the compiler from moving memory operations
+// across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Bijective blockIdx -> (vocab tile, row tile). Consecutive workgroups are
 // dealt round-robin to the 8 XCDs, so first undo that deal (each XCD gets a
-// contiguous run of logical ids), then walk logical ids in groups of 8 vocab
-// tiles: rows outer, vocab inner, so the workgroups resident on one XCD share
-// W tiles and hidden-state tiles through that XCD's L2.
+// contiguous run of logical ids), then walk logical ids in groups of
+// TIM_GROUP_V vocab tiles: rows outer, vocab inner, so the workgroups resident
+// on one XCD share W tiles and hidden-state tiles through that XCD's L2.
 __device__ __forceinline__ void tile_of(int bid, int nblk, int n_vt, int& vt, int& tt) {
   const int q = nblk >> 3, rem = nblk & 7;
   const int x = bid & 7, i = bid >> 3;
   const int lid = x * q + (x < rem ? x : rem) + i;
-  constexpr int GV = 8;
+  constexpr int GV = TIM_GROUP_V;
   const int n_tt = nblk / n_vt;
   const int group = lid / (GV * n_tt);
   const int first = group * GV;
@@ -91,32 +161,33 @@ __device__ __forceinline__ void tile_of(int bid, int nblk, int n_vt, int& vt, in
 // Per-lane byte offsets of this workgroup's DMA loads, relative to the tile's
 // first row at hidden index 0. They do not change along the hidden dimension:
 // each stage only moves the scalar offset.
-template <int NTB>
+template <int NTB, int WT>
 struct LoadPlan {
-  static constexpr int HB = Tile<NTB>::BT / 32;  // hidden-state blocks per wave
-  uint32_t w_off[8];
+  static constexpr int NW = Tile<NTB, WT>::NW;
+  static constexpr int WB = 4 * kChunks / NW;                       // W blocks of 1 KB per wave
+  static constexpr int HB = Tile<NTB, WT>::BT * kChunks / (64 * NW);  // hidden-state blocks per wave
+  static constexpr int L = WB + HB;                          // DMA loads per wave per stage
+  uint32_t w_off[WB];
   uint32_t h_off[HB];
 };
 
-template <int NTB>
-__device__ __forceinline__ LoadPlan<NTB> make_load_plan(int w_rows, int h_rows, int d, int wave,
+template <int NTB, int WT>
+__device__ __forceinline__ LoadPlan<NTB, WT> make_load_plan(int w_rows, int h_rows, int d, int wave,
                                                         int lane) {
-  LoadPlan<NTB> pl;
-  // W tile: 256 rows x 8 chunks = 32 blocks of 1 KB (64 lanes x 16 B); 8 per wave.
+  LoadPlan<NTB, WT> pl;
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int p = (wave * 8 + q) * 64 + lane;
-    int r = p >> 3;
-    const int c = (p & 7) ^ swz(r);
+  for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q) {
+    const int p = (wave * LoadPlan<NTB, WT>::WB + q) * 64 + lane;
+    int r = p / kChunks;
+    const int c = (p % kChunks) ^ swz(r);
     if (r >= w_rows) r = w_rows - 1;  // rows past V: a valid row, masked in the epilogue
     pl.w_off[q] = (uint32_t)(r * d + c * 8) * 2u;
   }
-  // Hidden-state tile: BT rows x 8 chunks = BT / 8 blocks.
 #pragma unroll
-  for (int q = 0; q < LoadPlan<NTB>::HB; ++q) {
-    const int p = (wave * LoadPlan<NTB>::HB + q) * 64 + lane;
-    int r = p >> 3;
-    const int c = (p & 7) ^ swz(r);
+  for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q) {
+    const int p = (wave * LoadPlan<NTB, WT>::HB + q) * 64 + lane;
+    int r = p / kChunks;
+    const int c = (p % kChunks) ^ swz(r);
     if (r >= h_rows) r = h_rows - 1;  // rows past the batch: never written out
     pl.h_off[q] = (uint32_t)(r * d + c * 8) * 2u;
   }
@@ -134,43 +205,64 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 #endif
 }
 
-template <int NTB>
-__device__ __forceinline__ void load_stage(unsigned char* lds, rsrc_t wr, rsrc_t hr,
-                                           const LoadPlan<NTB>& pl, int wave, int soff) {
+template <int NTB, int WT>
+__device__ __forceinline__ void load_stage(unsigned char* buf, rsrc_t wr, rsrc_t hr,
+                                           const LoadPlan<NTB, WT>& pl, int wave, int soff) {
 #if defined(__HIP_DEVICE_COMPILE__)
 #pragma unroll
-  for (int q = 0; q < 8; ++q)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(lds + (wave * 8 + q) * 1024), 16,
-                                             pl.w_off[q], soff, 0, 0);
-#pragma unroll
-  for (int q = 0; q < LoadPlan<NTB>::HB; ++q)
+  for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        hr, (lds_void*)(lds + kWBytes + (wave * LoadPlan<NTB>::HB + q) * 1024), 16, pl.h_off[q],
+        wr, (lds_void*)(buf + (wave * LoadPlan<NTB, WT>::WB + q) * 1024), 16, pl.w_off[q], soff, 0, 0);
+#pragma unroll
+  for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        hr, (lds_void*)(buf + kWBytes + (wave * LoadPlan<NTB, WT>::HB + q) * 1024), 16, pl.h_off[q],
         soff, 0, 0);
 #endif
 }
 
+// MFMA operands of one k-step: 4 W fragments (128 vocab rows) and NTB
+// hidden-state fragments (NTB * 32 rows), 8 bf16 per lane each.
 template <int NTB>
-__device__ __forceinline__ void compute_stage(const unsigned char* lds, f32x16 (&acc)[4][NTB],
-                                              int wv, int wt, int lane) {
+struct Frags {
+  bf16x8 a[4];
+  bf16x8 b[NTB];
+};
+
+template <int NTB>
+__device__ __forceinline__ void load_frags(const unsigned char* buf, int s, Frags<NTB>& f,
+                                           int wv, int wt, int lane) {
   const int r32 = lane & 31, hi = lane >> 5;
-  const int sw = swz(r32);  // every operand row is (multiple of 32) + r32
+  const int c = ((2 * s + hi) ^ swz(r32)) * 16;  // every operand row is (multiple of 32) + r32
 #pragma unroll
-  for (int s = 0; s < kKStage / 16; ++s) {
-    const int c = ((2 * s + hi) ^ sw) * 16;
-    bf16x8 a[4], b[NTB];
+  for (int bb = 0; bb < 4; ++bb)
+    f.a[bb] = *(const bf16x8*)(buf + (wv * 128 + bb * 32 + r32) * kRowBytes + c);
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-      a[bb] = *(const bf16x8*)(lds + (wv * 128 + bb * 32 + r32) * kRowBytes + c);
+  for (int j = 0; j < NTB; ++j)
+    f.b[j] = *(const bf16x8*)(buf + kWBytes + (wt * NTB * 32 + j * 32 + r32) * kRowBytes + c);
+}
+
+// Scheduling hints for one region of the main loop: spread NV vector-memory
+// loads and ND LDS reads among the NM MFMAs (one load and one read after each
+// MFMA while they last), so that no burst of loads backs up the vector-memory
+// queue behind which a wave's next MFMA would wait.
+template <int NM, int NV, int ND>
+__device__ __forceinline__ void interleave() {
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // 1 MFMA
+    if (i < NV) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);  // 1 VMEM
+    if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 DS read
+  }
+}
+
+template <int NTB>
+__device__ __forceinline__ void mma(const Frags<NTB>& f, f32x16 (&acc)[4][NTB]) {
+#pragma unroll
+  for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
     for (int j = 0; j < NTB; ++j)
-      b[j] = *(const bf16x8*)(lds + kWBytes + (wt * NTB * 32 + j * 32 + r32) * kRowBytes + c);
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-      for (int j = 0; j < NTB; ++j)
-        acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[bb], b[j], acc[bb][j], 0, 0, 0);
-  }
+      acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bb], f.b[j], acc[bb][j], 0, 0, 0);
 }
 
 // SPLITK4: after each quarter of the hidden dimension, fold the quarter's
@@ -187,12 +279,15 @@ __device__ __forceinline__ void quarter_fold(f32x16 (&acc)[4][NTB], f32x16 (&sum
     }
 }
 
-template <int NTB, bool SPLITK4, bool DUMP>
-__global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt) {
-  using TL = Tile<NTB>;
+template <int NTB, int WT, bool SPLITK4, bool DUMP>
+__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
+void lmhead_partials(LmHeadArgs a, int n_vt) {
+  using TL = Tile<NTB, WT>;
+  using LP = LoadPlan<NTB, WT>;
+  constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
   constexpr int BT = TL::BT;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds0[TL::kStageBytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char lds1[TL::kStageBytes];
+  constexpr int SB = TL::kStageBytes;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -213,33 +308,65 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
     for (int j = 0; j < NTB; ++j) acc[bb][j] = f32x16{};
   f32x16 sum[4][SPLITK4 ? NTB : 1];
 
-  const int nk = d / kKStage;
-  const int nk_q = nk / 4;
+  const int nk = d / kKS;   // stages
+  const int nk_q = nk / 4;  // stages per quarter (SPLITK4)
 
   const int w_rows = (V - v0) < kVocabTile ? (int)(V - v0) : kVocabTile;
   const int h_rows = (rows - t0) < BT ? (int)(rows - t0) : BT;
-  const LoadPlan<NTB> pl = make_load_plan<NTB>(w_rows, h_rows, d, wave, lane);
+  const LP pl = make_load_plan<NTB, WT>(w_rows, h_rows, d, wave, lane);
   const rsrc_t wr = make_rsrc(w + v0 * d, (uint64_t)w_rows * d * 2);
   const rsrc_t hr = make_rsrc(h + t0 * d, (uint64_t)h_rows * d * 2);
-  constexpr int kStep = kKStage * 2;  // bytes per stage along a row
+  constexpr int kStep = kKS * 2;  // bytes per stage along a row
 
-  // nk is even: each iteration consumes stage kt from lds0 and kt + 1 from lds1.
-  load_stage<NTB>(lds0, wr, hr, pl, wave, 0);
-  for (int kt = 0; kt < nk; kt += 2) {
-    wait_vmem();
-    __syncthreads();
-    load_stage<NTB>(lds1, wr, hr, pl, wave, (kt + 1) * kStep);
-    compute_stage<NTB>(lds0, acc, wv, wt, lane);
-    if constexpr (SPLITK4) {
-      if ((kt + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (kt + 1) / nk_q - 1);
+  // Software pipeline over stages, kNBuf LDS buffers, stage k in buffer k % kNBuf.
+  // Stage k + kNBuf - 1 is requested half-way through stage k, right after the
+  // barrier that (a) publishes stage k + 1 to every wave and (b) proves every
+  // wave is done with stage k - 1, whose buffer the new request overwrites.
+  // MFMA operands are read one k-step ahead, across the stage boundary too.
+#pragma unroll
+  for (int s = 0; s < kNBuf; ++s)
+    load_stage<NTB, WT>(lds + s * SB, wr, hr, pl, wave, (s < nk ? s : nk - 1) * kStep);
+  wait_vmem<(kNBuf - 1) * LP::L>();
+  __syncthreads();
+
+  Frags<NTB> f[2];
+  load_frags<NTB>(lds, 0, f[0], wv, wt, lane);
+  // The stage index of each request is clamped to the last stage, so the tail
+  // iterations re-read that stage into a buffer nobody reads again; this keeps
+  // the loop body free of branches and the wait counts uniform.
+  int k = 0;
+  for (; k + 1 < nk; ++k) {
+    unsigned char* cur = lds + (k % kNBuf) * SB;
+#pragma unroll
+    for (int s = 0; s + 1 < kSteps; ++s) {
+      load_frags<NTB>(cur, s + 1, f[(s + 1) & 1], wv, wt, lane);
+      mma<NTB>(f[s & 1], acc);
     }
-    wait_vmem();
-    __syncthreads();
-    if (kt + 2 < nk) load_stage<NTB>(lds0, wr, hr, pl, wave, (kt + 2) * kStep);
-    compute_stage<NTB>(lds1, acc, wv, wt, lane);
+    interleave<4 * NTB * (kSteps - 1), 0, (4 + NTB) * (kSteps - 1)>();
+    // Stage boundary, before the last k-step of stage k: this wave's reads of
+    // stage k are complete (its last fragments are in registers) and stage
+    // k + 1 has landed; after the barrier both hold for every wave, so stage
+    // k's buffer is refilled with stage k + kNBuf.
+    wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
+    stage_barrier();
+    const int kn = (k + kNBuf) < nk ? (k + kNBuf) : (nk - 1);
+    load_stage<NTB, WT>(cur, wr, hr, pl, wave, kn * kStep);
+    load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
+    mma<NTB>(f[(kSteps - 1) & 1], acc);
+    interleave<4 * NTB, LP::L, 4 + NTB>();
     if constexpr (SPLITK4) {
-      if ((kt + 2) % nk_q == 0) quarter_fold<NTB>(acc, sum, (kt + 2) / nk_q - 1);
+      if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
     }
+  }
+  {  // last stage: no boundary
+    const unsigned char* cur = lds + (k % kNBuf) * SB;
+#pragma unroll
+    for (int s = 0; s + 1 < kSteps; ++s) {
+      load_frags<NTB>(cur, s + 1, f[(s + 1) & 1], wv, wt, lane);
+      mma<NTB>(f[s & 1], acc);
+    }
+    mma<NTB>(f[(kSteps - 1) & 1], acc);
+    if constexpr (SPLITK4) quarter_fold<NTB>(acc, sum, 3);
   }
   if constexpr (SPLITK4) {
 #pragma unroll
@@ -247,7 +374,10 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
 #pragma unroll
       for (int j = 0; j < NTB; ++j) acc[bb][j] = sum[bb][j];
   }
-  __syncthreads();  // LDS stages are free; the epilogue reuses lds0
+  // The tail requests re-read the last stage; let them land before the
+  // epilogue reuses the first buffer.
+  wait_vmem<0>();
+  __syncthreads();  // every stage buffer is free; the epilogue reuses the first
 
   // ---------------------------------------------------------------- epilogue
   const int hi = lane >> 5, r32 = lane & 31;
@@ -255,7 +385,7 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
   // lane's vocab offset inside the tile for (block bb, register r):
   //   wv*128 + bb*32 + 8*(r>>2) + 4*hi + (r&3)
   const int64_t vlane = v0 + wv * 128 + 4 * hi;
-  float* red_m = (float*)lds0;           // [2][BT]
+  float* red_m = (float*)lds;            // [2][BT]
   float* red_s = red_m + 2 * BT;         // [2][BT]
   float* red_u = red_s + 2 * BT;         // [2][BT]
   float* zt_l = red_u + 2 * BT;          // [BT]
@@ -271,9 +401,13 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
     tok_loc[j] = (tok >= 0) ? (int)((int64_t)tok - vlane) : -1000000;
   }
 
-  // Phase A: temperature, vocab mask, tile max. z is formed from the
-  // accumulator by the same single multiply wherever it is needed, so the
-  // accumulators stay in their registers and every use sees the same bits.
+  // Phase A: temperature (z = acc * inv_tau, written back in place so every
+  // later use reads the same bits; a multiply by exactly 1 is skipped, which
+  // changes nothing), vocabulary mask (tail tile only: entries past V become
+  // -inf) and the row's max over the tile. Whether a tile is the tail depends
+  // only on (v0, V), so a tile takes the same path in every launch shape.
+  const bool full = v0 + kVocabTile <= V;
+  const bool scale = inv_tau != 1.0f;
 #pragma unroll
   for (int j = 0; j < NTB; ++j) {
     float mx = kNegInf;
@@ -281,21 +415,37 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
     for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int off = bb * 32 + 8 * (r >> 2) + (r & 3);
-        const float z = (vlane + off < V) ? acc[bb][j][r] * inv_tau : kNegInf;
+        float z = acc[bb][j][r];
+        if (scale) z = z * inv_tau;
+        if (!full && vlane + (bb * 32 + 8 * (r >> 2) + (r & 3)) >= V) z = kNegInf;
+        acc[bb][j][r] = z;
         mx = fmaxf(mx, z);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    if (hi == 0) red_m[wv * BT + wt * NTB * 32 + j * 32 + r32] = mx;
+    const int t_loc = wt * NTB * 32 + j * 32 + r32;
+    if (hi == 0) red_m[wv * BT + t_loc] = mx;
+    // Token gather: the row's token lies in this lane's 64 entries only for
+    // offsets tl in [0, 128) with bit 2 clear (the other lane half holds the
+    // rest). Rare, so the 64-way select runs under a divergent branch.
+    const int tl = tok_loc[j];
+    if (tl >= 0 && tl < 128 && ((tl >> 2) & 1) == 0) {
+      float zf = 0.f;
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (bb * 32 + 8 * (r >> 2) + (r & 3) == tl) zf = acc[bb][j][r];
+      zt_l[t_loc] = zf;
+    }
     if constexpr (DUMP) {
-      const int64_t tg = t0 + wt * NTB * 32 + j * 32 + r32;
+      const int64_t tg = t0 + t_loc;
       if (row_ok[j]) {
 #pragma unroll
         for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int64_t v = vlane + bb * 32 + 8 * (r >> 2) + (r & 3);
-            if (v < V) a.logits[tg * (int64_t)V + v] = acc[bb][j][r] * inv_tau;
+            if (v < V) a.logits[tg * (int64_t)V + v] = acc[bb][j][r];
           }
       }
     }
@@ -303,28 +453,38 @@ __global__ __launch_bounds__(256, 1) void lmhead_partials(LmHeadArgs a, int n_vt
   if constexpr (DUMP) return;
   __syncthreads();
 
-  // Phase B: sums against the tile max, in fixed (bb, r) order; token gather.
+  // Phase B: s = sum e^(z - M) and u = sum e^(z - M) (z - M) against the
+  // tile max M, in fixed (bb, r) order. In the tail tile the masked entries
+  // add exactly zero to both, so valid entries see the same arithmetic as in
+  // a full tile.
 #pragma unroll
   for (int j = 0; j < NTB; ++j) {
     const int t_loc = wt * NTB * 32 + j * 32 + r32;
     const float M = fmaxf(red_m[t_loc], red_m[BT + t_loc]);
     float s = 0.f, u = 0.f;
-    float zfound = 0.f;
-    bool found = false;
+    if (full) {
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
+      for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int off = bb * 32 + 8 * (r >> 2) + (r & 3);
-        const float z = (vlane + off < V) ? acc[bb][j][r] * inv_tau : kNegInf;
-        float x = z - M;
-        float e = exp2_hw(x * kLog2e);
-        if (z == kNegInf) { x = 0.f; e = 0.f; }
-        s = s + e;
-        u = __builtin_fmaf(e, x, u);
-        if (tok_loc[j] == off) { zfound = z; found = true; }
-      }
-    if (found) zt_l[t_loc] = zfound;
+        for (int r = 0; r < 16; ++r) {
+          const float x = acc[bb][j][r] - M;
+          const float e = exp2_hw(x * kLog2e);
+          s = s + e;
+          u = __builtin_fmaf(e, x, u);
+        }
+    } else {
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float z = acc[bb][j][r];
+          float x = z - M;
+          float e = exp2_hw(x * kLog2e);
+          if (z == kNegInf) { x = 0.f; e = 0.f; }
+          s = s + e;
+          u = __builtin_fmaf(e, x, u);
+        }
+    }
     s = s + __shfl_xor(s, 32);
     u = u + __shfl_xor(u, 32);
     if (hi == 0) {
@@ -438,28 +598,36 @@ __global__ __launch_bounds__(256) void lmhead_merge_fold(const Partial* __restri
 
 int n_vocab_tiles(int V) { return (V + kVocabTile - 1) / kVocabTile; }
 
-template <int NTB, bool SPLITK4, bool DUMP>
+template <int NTB, int WT, bool SPLITK4, bool DUMP>
 static hipError_t launch_partials_t(const LmHeadArgs& a, hipStream_t s) {
   const int n_vt = n_vocab_tiles(a.V);
-  const int64_t n_tt = (a.rows + Tile<NTB>::BT - 1) / Tile<NTB>::BT;
+  constexpr int BT = Tile<NTB, WT>::BT;
+  const int64_t n_tt = (a.rows + BT - 1) / BT;
   const int64_t nblk = n_tt * n_vt;
   if (nblk > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((lmhead_partials<NTB, SPLITK4, DUMP>), dim3((unsigned)nblk), dim3(256), 0, s,
-                     a, n_vt);
+  hipLaunchKernelGGL((lmhead_partials<NTB, WT, SPLITK4, DUMP>), dim3((unsigned)nblk), dim3(128 * WT), 0,
+                     s, a, n_vt);
   return hipGetLastError();
 }
 
-hipError_t launch_partials(const LmHeadArgs& a, int token_blocks, bool splitk4, hipStream_t s) {
+hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, hipStream_t s) {
   const bool dump = a.logits != nullptr;
-  if (splitk4) {
-    if (token_blocks >= 2)
-      return dump ? launch_partials_t<2, true, true>(a, s) : launch_partials_t<2, true, false>(a, s);
-    return dump ? launch_partials_t<1, true, true>(a, s) : launch_partials_t<1, true, false>(a, s);
+  if (splitk4) {  // a second accumulator set: at most 128 rows, 4 waves
+    if (rows_per_wg >= 128)
+      return dump ? launch_partials_t<2, 2, true, true>(a, s) : launch_partials_t<2, 2, true, false>(a, s);
+    return dump ? launch_partials_t<1, 2, true, true>(a, s) : launch_partials_t<1, 2, true, false>(a, s);
   }
-  switch (token_blocks) {
-    case 1: return dump ? launch_partials_t<1, false, true>(a, s) : launch_partials_t<1, false, false>(a, s);
-    case 2: return dump ? launch_partials_t<2, false, true>(a, s) : launch_partials_t<2, false, false>(a, s);
-    default: return dump ? launch_partials_t<4, false, true>(a, s) : launch_partials_t<4, false, false>(a, s);
+  switch (rows_per_wg) {
+    case 64: return dump ? launch_partials_t<1, 2, false, true>(a, s) : launch_partials_t<1, 2, false, false>(a, s);
+    case 128: return dump ? launch_partials_t<2, 2, false, true>(a, s) : launch_partials_t<2, 2, false, false>(a, s);
+    default:
+#if TIM_TRAIN_ROWS == 128
+      return dump ? launch_partials_t<2, 2, false, true>(a, s) : launch_partials_t<2, 2, false, false>(a, s);
+#elif TIM_WIDE_WAVES
+      return dump ? launch_partials_t<2, 4, false, true>(a, s) : launch_partials_t<2, 4, false, false>(a, s);
+#else
+      return dump ? launch_partials_t<4, 2, false, true>(a, s) : launch_partials_t<4, 2, false, false>(a, s);
+#endif
   }
 }
 

@@ -19,12 +19,12 @@ inline float inv_temperature(float temperature) {
   return (float)(1.0 / (double)temperature);
 }
 
-// Row tile (in 32-row blocks per wave) for a launch of `rows` rows.
-inline int token_blocks_for(int64_t rows, int32_t mode, bool splitk4) {
-  int tb = 4;
-  if (mode == TIM_MODE_ROLLOUT) tb = rows <= 64 ? 1 : (rows <= 128 ? 2 : 4);
-  if (splitk4 && tb > 2) tb = 2;  // the split-K engine keeps a second accumulator set
-  return tb;
+// Rows per workgroup for a launch of `rows` rows.
+inline int row_tile_for(int64_t rows, int32_t mode, bool splitk4) {
+  int rt = 256;
+  if (mode == TIM_MODE_ROLLOUT) rt = rows <= 64 ? 64 : (rows <= 128 ? 128 : 256);
+  if (splitk4 && rt > 128) rt = 128;  // the split-K engine keeps a second accumulator set
+  return rt;
 }
 
 }  // namespace
@@ -47,7 +47,7 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
 
   const bool splitk4 = order == TIM_ORDER_SPLITK4;
   const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
-  const int tb = token_blocks_for(step, mode, splitk4);
+  const int tb = row_tile_for(step, mode, splitk4);
   const float inv_tau = inv_temperature(temperature);
   const __bf16* h = (const __bf16*)hidden;
   tim::Partial* part = (tim::Partial*)workspace;
@@ -93,7 +93,7 @@ tim_status tim_logprobs_partials(const void* hidden, const void* w_vocab, const 
   a.inv_tau = inv_temperature(temperature);
   a.part = (tim::Partial*)workspace;
   a.logits = nullptr;
-  return hip_status(tim::launch_partials(a, token_blocks_for(T, mode, splitk4), splitk4, stream));
+  return hip_status(tim::launch_partials(a, row_tile_for(T, mode, splitk4), splitk4, stream));
 }
 
 tim_status tim_logprobs_merge(const void* workspace, const int32_t* tokens, int64_t T, int32_t V,
@@ -131,7 +131,7 @@ tim_status tim_logits(const void* hidden, const void* w_vocab, int64_t T, int32_
   a.inv_tau = inv_temperature(temperature);
   a.part = nullptr;
   a.logits = logits;
-  return hip_status(tim::launch_partials(a, splitk4 ? 2 : 4, splitk4, stream));
+  return hip_status(tim::launch_partials(a, 128, splitk4, stream));
 }
 
 const char* tim_status_string(tim_status s) {
