@@ -91,7 +91,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="mid")
-    ap.add_argument("--cpu-rows", type=int, default=2048, help="rows of the oracle CPU baseline (0 = skip)")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="rows of the oracle CPU baseline (0 = skip)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, run a plain copy kernel of known size (torch.neg over 2^28 fp32: "
                          "1 GiB read + 1 GiB written) so a counter profile can scale HBM byte counters")

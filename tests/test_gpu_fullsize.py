@@ -1,0 +1,148 @@
+"""Full-size workloads on the GPU, in the launch configurations the benchmark
+uses, checked against the fp64 oracle on seeded row samples, plus bitwise
+batch invariance across every batching the workloads name and the
+controlled-mismatch report between the invariant path and the split-K4 engine.
+
+Shapes (synthetic, seeded; see workload.gen):
+  small  d=2048, V=151936, 16 responses U[128,1024] packed, one training call
+  mid    d=4096, V=151936, 64 responses U[512,4096] packed, micro-batches of 16384
+  stress the mid stream evaluated in rollout groupings of random size 1..256
+         (shuffled) and training micro-batches 4096 / 16384 / 65536; split-K4
+         engine supplies the second log-probs for the mismatch statistics
+  long   d=5120, V=152064, 8 x 16384 tokens, tau = 0.7, micro-batches of 32768
+         and rollout decode batches of 64
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_14220_amd as tim
+from paper_2605_14220_amd import Mode, Order
+from tim_testutil import TOL_ENT, TOL_LOGP, TOL_W_REL, bits_equal, check_close, require_gpu
+from workload import CONFIGS, bf16_bits, hidden_states, uniforms, vocab_weights
+from workload.gen import seeds
+from workload.sampler import sample_tokens
+
+pytestmark = pytest.mark.gpu
+SAMPLE_ROWS = 48
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+_cache = {}
+
+
+def workload(name):
+    """Inputs of a named configuration, drawn once per test session on the GPU."""
+    if name in _cache:
+        return _cache[name]
+    _cache.clear()
+    torch.cuda.empty_cache()
+    cfg = CONFIGS[name]
+    hs, ws, us = seeds(cfg)
+    T = cfg.tokens
+    print(f"[fullsize] drawing {name}: T={T} d={cfg.d} V={cfg.V} tau={cfg.temperature}", flush=True)
+    h = hidden_states(T, cfg.d, hs, device="cuda")
+    W = vocab_weights(cfg.V, cfg.d, cfg.w_std, ws, device="cuda")
+    tok = sample_tokens(h, W, cfg.temperature, uniforms(T, us), dtype=torch.float32)
+    torch.cuda.synchronize()
+    _cache[name] = (cfg, h, W, tok)
+    return _cache[name]
+
+
+def oracle_sample(cfg, h, W, tok, lp, H, seed=7):
+    T = h.shape[0]
+    rows = np.sort(np.random.default_rng(seed).choice(T, size=min(SAMPLE_ROWS, T), replace=False))
+    idx = torch.as_tensor(rows, device="cuda")
+    ref_lp, ref_H = oracle.logprobs(bf16_bits(h.index_select(0, idx)), bf16_bits(W),
+                                    tok.index_select(0, idx).cpu().numpy(), cfg.temperature)
+    check_close(f"{cfg.name} logp ({len(rows)} sampled rows)", lp, ref_lp, TOL_LOGP, rows)
+    check_close(f"{cfg.name} entropy ({len(rows)} sampled rows)", H, ref_H, TOL_ENT, rows)
+    # statistical pins of the sampled workload: E[logp(sampled)] = -E[H]
+    lpn, Hn = lp.double().cpu().numpy(), H.double().cpu().numpy()
+    assert abs(lpn.mean() + Hn.mean()) < 6 * lpn.std() / math.sqrt(T)
+    assert (Hn >= 0).all() and (Hn <= math.log(cfg.V) + 1e-4).all() and (lpn <= 1e-6).all()
+    return ref_lp, ref_H
+
+
+def test_small_one_packed_call():
+    cfg, h, W, tok = workload("small")
+    lp, H, _ = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=0)
+    oracle_sample(cfg, h, W, tok, lp, H)
+
+
+def test_mid_micro_batches():
+    cfg, h, W, tok = workload("mid")
+    lp, H, _ = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=cfg.micro_batch)
+    oracle_sample(cfg, h, W, tok, lp, H)
+    # mean entropy of this synthetic workload: ln V - sigma_z^2 / 2, sigma_z = 0.02 sqrt(d)
+    sig2 = (0.02 ** 2) * cfg.d
+    assert abs(H.double().mean().item() - (math.log(cfg.V) - sig2 / 2)) < 0.05
+
+
+def test_stress_invariance_and_mismatch_report():
+    cfg, h, W, tok = workload("stress")
+    T = h.shape[0]
+    ref = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=16384, lse=True)
+    for mb in (4096, 65536):
+        out = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=mb, lse=True)
+        for x, y in zip(out, ref):
+            assert bits_equal(x, y), f"micro-batch {mb} differs"
+    # rollout: every row once, in shuffled decode batches of random size 1..256
+    rng = np.random.default_rng(44)
+    perm = torch.as_tensor(rng.permutation(T), device="cuda")
+    got = [torch.empty_like(ref[i]) for i in range(3)]
+    i = calls = 0
+    while i < T:
+        n = int(rng.integers(1, 257))
+        rows = perm[i:i + n]
+        out = tim.logprobs(h.index_select(0, rows), W, tok.index_select(0, rows), cfg.temperature,
+                           mode=Mode.ROLLOUT, lse=True)
+        for g, o in zip(got, out):
+            g[rows] = o
+        i += n
+        calls += 1
+    for x, y in zip(got, ref):
+        assert bits_equal(x, y), "rollout groupings differ from training"
+    print(f"[stress] {calls} rollout calls + micro-batches 4096/16384/65536: all {T} rows bitwise equal")
+    # second engine: split-K4 reduction order
+    eng = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=16384, order=Order.SPLITK4)
+    oracle_sample(cfg, h, W, tok, eng[0], eng[1], seed=8)
+    lr, k3, w = tim.mismatch(ref[0], eng[0], 2.0)
+    d = lr.abs().double()
+    q = torch.quantile(d[: 1 << 24].float(), torch.tensor([0.5, 0.99], device="cuda")).tolist()
+    print(f"[stress] |dlogp| p50={q[0]:.3e} p99={q[1]:.3e} max={d.max().item():.3e}; mean k3="
+          f"{k3.double().mean().item():.3e}; IS weight (C=2) mean={w.double().mean().item():.9f} "
+          f"min={w.min().item():.7f} max={w.max().item():.7f}; rows differing in bits: "
+          f"{(lr != 0).double().mean().item():.3f}")
+    # the engines agree within the oracle tolerance, so every weight is within 2e-3 of 1
+    assert d.max().item() < 2 * TOL_LOGP
+    assert ((w - 1).abs() <= 2 * TOL_W_REL).all()
+    r_lr, r_k3, r_w = oracle.mismatch(ref[0].cpu().numpy(), eng[0].cpu().numpy(), 2.0)
+    assert np.all(np.abs(lr.double().cpu().numpy() - r_lr) <= 2.0 ** -24 * np.abs(r_lr) + 1e-45)
+    assert np.all(np.abs(w.double().cpu().numpy() - r_w) <= TOL_W_REL * r_w)
+
+
+def test_long_training_vs_decode_batches():
+    cfg, h, W, tok = workload("long")
+    T = h.shape[0]
+    lp, H, lse = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=cfg.micro_batch,
+                              lse=True)
+    oracle_sample(cfg, h, W, tok, lp, H)
+    # rollout pass: decode batches of 64 rows
+    B = cfg.rollout_batch
+    ws = torch.empty(tim.workspace_size(B, cfg.d, cfg.V, Mode.ROLLOUT), dtype=torch.uint8, device="cuda")
+    got = [torch.empty_like(lp), torch.empty_like(H), torch.empty_like(lse)]
+    for t0 in range(0, T, B):
+        sl = slice(t0, min(T, t0 + B))
+        tim.logprobs(h[sl], W, tok[sl], cfg.temperature, mode=Mode.ROLLOUT, lse=True, workspace=ws,
+                     out=(got[0][sl], got[1][sl], got[2][sl]))
+    assert bits_equal(got[0], lp) and bits_equal(got[1], H) and bits_equal(got[2], lse)
+    print(f"[long] {T // B} decode batches of {B} rows bitwise equal to micro-batches of {cfg.micro_batch}")
