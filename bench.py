@@ -193,6 +193,31 @@ def main(argv=None):
         f"{tok_per_s:,.0f} tokens/s, path {path_tflops:.1f} TFLOP/s = {path_tflops / PEAK_BF16_TFLOPS:.1%} of "
         f"bf16 peak; partials kernel {avg_ms:.3f} ms/launch = {achieved_tflops:.1f} TFLOP/s")
 
+    # rollout mode (decode steps): each call streams all of W once; HBM-bound
+    B = 64
+    rws = torch.empty(tim.workspace_size(B, d, V, Mode.ROLLOUT), dtype=torch.uint8, device=dev)
+    r_out = tuple(torch.empty(B, dtype=torch.float32, device=dev) for _ in range(3))
+    n_calls = 40
+    for i in range(3):
+        tim.logprobs(h[i * B:(i + 1) * B], W, tok[i * B:(i + 1) * B], tau, mode=Mode.ROLLOUT, lse=True,
+                     workspace=rws, out=r_out)
+    r0 = torch.cuda.Event(enable_timing=True)
+    r1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    r0.record(stream)
+    for i in range(n_calls):
+        a0 = (i * B) % (T - B)
+        tim.logprobs(h[a0:a0 + B], W, tok[a0:a0 + B], tau, mode=Mode.ROLLOUT, lse=True, workspace=rws, out=r_out)
+    r1.record(stream)
+    torch.cuda.synchronize()
+    r_ms = r0.elapsed_time(r1) / n_calls
+    r_bytes = 2.0 * V * d + 2.0 * B * d + 4 * B + 16.0 * B * ((V + 255) // 256) * 2 + 12 * B
+    rollout = {"rows_per_call": B, "ms_per_call": r_ms, "tokens_per_s": B / (r_ms / 1e3),
+               "bound": "hbm", "achieved_GBps": r_bytes / (r_ms / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
+               "frac": r_bytes / (r_ms / 1e3) / 1e9 / PEAK_HBM_GBS, "bytes_per_call": r_bytes}
+    log(f"[bench] rollout decode batch of {B}: {r_ms:.3f} ms/call (partials + merge), "
+        f"{rollout['achieved_GBps']:.0f} GB/s algorithmic = {rollout['frac']:.1%} of 8 TB/s")
+
     if args.calibrate_copy:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -248,6 +273,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "parity_sample": parity,
         "mismatch_vs_splitk4": mis,
+        "rollout_decode": rollout,
     }
     print(json.dumps(out), flush=True)
 
