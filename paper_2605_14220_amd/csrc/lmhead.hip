@@ -66,6 +66,12 @@ struct rsrc_t {
 #ifndef TIM_GROUP_V
 #define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
 #endif
+#ifndef TIM_LOAD_AUX
+#define TIM_LOAD_AUX 0     // cache-policy bits of the global->LDS loads (gfx950 sc0=1, nt=2, sc1=16)
+#endif
+#ifndef TIM_PERSISTENT
+#define TIM_PERSISTENT 1   // full-size launches: one workgroup per CU looping over tiles
+#endif
 #ifndef TIM_TRAIN_ROWS
 #define TIM_TRAIN_ROWS 256 // row tile of full-size launches: 256 (one workgroup per CU) or 128 (two)
 #endif
@@ -139,17 +145,13 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Bijective blockIdx -> (vocab tile, row tile). Consecutive workgroups are
-// dealt round-robin to the 8 XCDs, so first undo that deal (each XCD gets a
-// contiguous run of logical ids), then walk logical ids in groups of
-// TIM_GROUP_V vocab tiles: rows outer, vocab inner, so the workgroups resident
-// on one XCD share W tiles and hidden-state tiles through that XCD's L2.
-__device__ __forceinline__ void tile_of(int bid, int nblk, int n_vt, int& vt, int& tt) {
-  const int q = nblk >> 3, rem = nblk & 7;
-  const int x = bid & 7, i = bid >> 3;
-  const int lid = x * q + (x < rem ? x : rem) + i;
+// Tile order: logical id -> (vocab tile, row tile), walking groups of
+// TIM_GROUP_V vocab tiles with the row tiles outer and the vocab tiles inner,
+// so that the workgroups resident on one XCD at a time (consecutive logical
+// ids, see lmhead_partials) share W tiles and hidden-state tiles through that
+// XCD's L2.
+__device__ __forceinline__ void tile_of_lid(int lid, int n_vt, int n_tt, int& vt, int& tt) {
   constexpr int GV = TIM_GROUP_V;
-  const int n_tt = nblk / n_vt;
   const int group = lid / (GV * n_tt);
   const int first = group * GV;
   const int gv = (n_vt - first) < GV ? (n_vt - first) : GV;
@@ -212,12 +214,13 @@ __device__ __forceinline__ void load_stage(unsigned char* buf, rsrc_t wr, rsrc_t
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        wr, (lds_void*)(buf + (wave * LoadPlan<NTB, WT>::WB + q) * 1024), 16, pl.w_off[q], soff, 0, 0);
+        wr, (lds_void*)(buf + (wave * LoadPlan<NTB, WT>::WB + q) * 1024), 16, pl.w_off[q], soff, 0,
+        TIM_LOAD_AUX);
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(
         hr, (lds_void*)(buf + kWBytes + (wave * LoadPlan<NTB, WT>::HB + q) * 1024), 16, pl.h_off[q],
-        soff, 0, 0);
+        soff, 0, TIM_LOAD_AUX);
 #endif
 }
 
@@ -279,113 +282,23 @@ __device__ __forceinline__ void quarter_fold(f32x16 (&acc)[4][NTB], f32x16 (&sum
     }
 }
 
-template <int NTB, int WT, bool SPLITK4, bool DUMP>
-__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
-void lmhead_partials(LmHeadArgs a, int n_vt) {
-  using TL = Tile<NTB, WT>;
-  using LP = LoadPlan<NTB, WT>;
-  constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
-  constexpr int BT = TL::BT;
-  constexpr int SB = TL::kStageBytes;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB];
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+// One tile's per-row results from its accumulators (see the file comment):
+// phase A scales, masks and finds each row's tile max and gathers the token's
+// logit, phase B sums against that max, phase C combines the two vocab waves
+// and stores one Partial per row. `scratch` holds 7 * BT floats of LDS.
+template <int NTB, int WT, bool DUMP>
+__device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int vt, int64_t v0, int64_t t0,
+                                              f32x16 (&acc)[4][NTB], float* scratch, int wave, int lane) {
+  constexpr int BT = Tile<NTB, WT>::BT;
   const int wv = wave & 1, wt = wave >> 1;
-  int vt, tt;
-  tile_of(blockIdx.x, gridDim.x, n_vt, vt, tt);
-  const int64_t v0 = (int64_t)vt * kVocabTile;
-  const int64_t t0 = (int64_t)tt * BT;
-  const __bf16* __restrict__ w = (const __bf16*)a.w;
-  const __bf16* __restrict__ h = (const __bf16*)a.hidden;
-  const int d = a.d, V = a.V;
+  const int V = a.V;
   const int64_t rows = a.rows;
-
-  f32x16 acc[4][NTB];
-#pragma unroll
-  for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-    for (int j = 0; j < NTB; ++j) acc[bb][j] = f32x16{};
-  f32x16 sum[4][SPLITK4 ? NTB : 1];
-
-  const int nk = d / kKS;   // stages
-  const int nk_q = nk / 4;  // stages per quarter (SPLITK4)
-
-  const int w_rows = (V - v0) < kVocabTile ? (int)(V - v0) : kVocabTile;
-  const int h_rows = (rows - t0) < BT ? (int)(rows - t0) : BT;
-  const LP pl = make_load_plan<NTB, WT>(w_rows, h_rows, d, wave, lane);
-  const rsrc_t wr = make_rsrc(w + v0 * d, (uint64_t)w_rows * d * 2);
-  const rsrc_t hr = make_rsrc(h + t0 * d, (uint64_t)h_rows * d * 2);
-  constexpr int kStep = kKS * 2;  // bytes per stage along a row
-
-  // Software pipeline over stages, kNBuf LDS buffers, stage k in buffer k % kNBuf.
-  // Stage k + kNBuf - 1 is requested half-way through stage k, right after the
-  // barrier that (a) publishes stage k + 1 to every wave and (b) proves every
-  // wave is done with stage k - 1, whose buffer the new request overwrites.
-  // MFMA operands are read one k-step ahead, across the stage boundary too.
-#pragma unroll
-  for (int s = 0; s < kNBuf; ++s)
-    load_stage<NTB, WT>(lds + s * SB, wr, hr, pl, wave, (s < nk ? s : nk - 1) * kStep);
-  wait_vmem<(kNBuf - 1) * LP::L>();
-  __syncthreads();
-
-  Frags<NTB> f[2];
-  load_frags<NTB>(lds, 0, f[0], wv, wt, lane);
-  // The stage index of each request is clamped to the last stage, so the tail
-  // iterations re-read that stage into a buffer nobody reads again; this keeps
-  // the loop body free of branches and the wait counts uniform.
-  int k = 0;
-  for (; k + 1 < nk; ++k) {
-    unsigned char* cur = lds + (k % kNBuf) * SB;
-#pragma unroll
-    for (int s = 0; s + 1 < kSteps; ++s) {
-      load_frags<NTB>(cur, s + 1, f[(s + 1) & 1], wv, wt, lane);
-      mma<NTB>(f[s & 1], acc);
-    }
-    interleave<4 * NTB * (kSteps - 1), 0, (4 + NTB) * (kSteps - 1)>();
-    // Stage boundary, before the last k-step of stage k: this wave's reads of
-    // stage k are complete (its last fragments are in registers) and stage
-    // k + 1 has landed; after the barrier both hold for every wave, so stage
-    // k's buffer is refilled with stage k + kNBuf.
-    wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
-    stage_barrier();
-    const int kn = (k + kNBuf) < nk ? (k + kNBuf) : (nk - 1);
-    load_stage<NTB, WT>(cur, wr, hr, pl, wave, kn * kStep);
-    load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
-    mma<NTB>(f[(kSteps - 1) & 1], acc);
-    interleave<4 * NTB, LP::L, 4 + NTB>();
-    if constexpr (SPLITK4) {
-      if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
-    }
-  }
-  {  // last stage: no boundary
-    const unsigned char* cur = lds + (k % kNBuf) * SB;
-#pragma unroll
-    for (int s = 0; s + 1 < kSteps; ++s) {
-      load_frags<NTB>(cur, s + 1, f[(s + 1) & 1], wv, wt, lane);
-      mma<NTB>(f[s & 1], acc);
-    }
-    mma<NTB>(f[(kSteps - 1) & 1], acc);
-    if constexpr (SPLITK4) quarter_fold<NTB>(acc, sum, 3);
-  }
-  if constexpr (SPLITK4) {
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-      for (int j = 0; j < NTB; ++j) acc[bb][j] = sum[bb][j];
-  }
-  // The tail requests re-read the last stage; let them land before the
-  // epilogue reuses the first buffer.
-  wait_vmem<0>();
-  __syncthreads();  // every stage buffer is free; the epilogue reuses the first
-
-  // ---------------------------------------------------------------- epilogue
   const int hi = lane >> 5, r32 = lane & 31;
   const float inv_tau = a.inv_tau;
   // lane's vocab offset inside the tile for (block bb, register r):
   //   wv*128 + bb*32 + 8*(r>>2) + 4*hi + (r&3)
   const int64_t vlane = v0 + wv * 128 + 4 * hi;
-  float* red_m = (float*)lds;            // [2][BT]
+  float* red_m = scratch;                // [2][BT]
   float* red_s = red_m + 2 * BT;         // [2][BT]
   float* red_u = red_s + 2 * BT;         // [2][BT]
   float* zt_l = red_u + 2 * BT;          // [BT]
@@ -407,20 +320,30 @@ void lmhead_partials(LmHeadArgs a, int n_vt) {
   // -inf) and the row's max over the tile. Whether a tile is the tail depends
   // only on (v0, V), so a tile takes the same path in every launch shape.
   const bool full = v0 + kVocabTile <= V;
-  const bool scale = inv_tau != 1.0f;
+  if (inv_tau != 1.0f) {
+#pragma unroll
+    for (int j = 0; j < NTB; ++j)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[bb][j][r] = acc[bb][j][r] * inv_tau;
+  }
+  if (!full) {
+#pragma unroll
+    for (int j = 0; j < NTB; ++j)
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (vlane + (bb * 32 + 8 * (r >> 2) + (r & 3)) >= V) acc[bb][j][r] = kNegInf;
+  }
 #pragma unroll
   for (int j = 0; j < NTB; ++j) {
     float mx = kNegInf;
 #pragma unroll
     for (int bb = 0; bb < 4; ++bb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float z = acc[bb][j][r];
-        if (scale) z = z * inv_tau;
-        if (!full && vlane + (bb * 32 + 8 * (r >> 2) + (r & 3)) >= V) z = kNegInf;
-        acc[bb][j][r] = z;
-        mx = fmaxf(mx, z);
-      }
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[bb][j][r]);
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     const int t_loc = wt * NTB * 32 + j * 32 + r32;
     if (hi == 0) red_m[wv * BT + t_loc] = mx;
@@ -512,6 +435,196 @@ void lmhead_partials(LmHeadArgs a, int n_vt) {
   }
 }
 
+template <int NTB, int WT>
+struct TileCtx {
+  int vt;
+  int64_t v0, t0;
+  LoadPlan<NTB, WT> pl;
+  rsrc_t wr, hr;
+};
+
+template <int NTB, int WT>
+__device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int lid, int n_vt, int n_tt,
+                                                      int wave, int lane) {
+  constexpr int BT = Tile<NTB, WT>::BT;
+  // Opaque copies: every call recomputes its context instead of the compiler
+  // reusing (and keeping live) the result of an earlier call.
+  asm volatile("" : "+s"(lid));
+  asm volatile("" : "+v"(lane));
+  TileCtx<NTB, WT> c;
+  int tt;
+  tile_of_lid(lid, n_vt, n_tt, c.vt, tt);
+  c.v0 = (int64_t)c.vt * kVocabTile;
+  c.t0 = (int64_t)tt * BT;
+  const int w_rows = (a.V - c.v0) < kVocabTile ? (int)(a.V - c.v0) : kVocabTile;
+  const int h_rows = (a.rows - c.t0) < BT ? (int)(a.rows - c.t0) : BT;
+  c.pl = make_load_plan<NTB, WT>(w_rows, h_rows, a.d, wave, lane);
+  c.wr = make_rsrc((const __bf16*)a.w + c.v0 * a.d, (uint64_t)w_rows * a.d * 2);
+  c.hr = make_rsrc((const __bf16*)a.hidden + c.t0 * a.d, (uint64_t)h_rows * a.d * 2);
+  return c;
+}
+
+// Partials of a sequence of (vocab tile, row tile) output tiles. The logical
+// tile ids are dealt to the 8 XCDs in contiguous chunks, and within an XCD
+// round-robin to its workgroups, so at any time the workgroups of one XCD work
+// on consecutive ids. With one workgroup per tile this is a plain launch; with
+// a grid of one workgroup per CU it is persistent, and the stage pipeline then
+// runs on across tiles: the last stage boundaries of a tile already request
+// the next tile's first stages, which land while this tile's epilogue runs.
+template <int NTB, int WT, bool SPLITK4, bool DUMP>
+__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
+void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
+  using TL = Tile<NTB, WT>;
+  using LP = LoadPlan<NTB, WT>;
+  using TC = TileCtx<NTB, WT>;
+  constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
+  constexpr int BT = TL::BT;
+  constexpr int SB = TL::kStageBytes;
+  constexpr int EPI = 7 * BT * 4;
+  // Epilogue scratch of its own when it fits, so the next tile's stages can
+  // land during the epilogue; otherwise it reuses the first stage buffer.
+  constexpr bool kSep = kNBuf * SB + EPI <= (160 * 1024) / Shape<NTB, WT, SPLITK4>::PER_CU;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB + (kSep ? EPI : 0)];
+  float* scratch = (float*)(kSep ? lds + kNBuf * SB : lds);
+
+  const int lane0 = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wv = wave & 1, wt = wave >> 1;
+
+  // this workgroup's tiles: start + wi, start + wi + w_x, ... below start + t_x
+  const int n_tiles = n_vt * n_tt;
+  const int x = blockIdx.x & 7, wi = blockIdx.x >> 3;
+  const int w_x = (int)(gridDim.x >> 3) + (x < (int)(gridDim.x & 7) ? 1 : 0);
+  const int tq = n_tiles >> 3, trm = n_tiles & 7;
+  const int t_x = tq + (x < trm ? 1 : 0);
+  const int start = x * tq + (x < trm ? x : trm);
+  int j = wi;
+  if (j >= t_x) return;
+
+  const int nk = a.d / kKS;  // stages per tile; a multiple of kNBuf
+  const int nk_q = nk / 4;   // stages per quarter (SPLITK4)
+  constexpr int kStep = kKS * 2;
+
+  TC cur = make_tile<NTB, WT>(a, start + j, n_vt, n_tt, wave, lane0);
+
+#pragma unroll
+  for (int s = 0; s < kNBuf; ++s)
+    load_stage<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep);
+
+  f32x16 acc[4][NTB];
+  f32x16 sum[4][SPLITK4 ? NTB : 1];
+  Frags<NTB> f[2];
+  while (true) {
+    // Per-tile lane arithmetic is recomputed inside the loop rather than
+    // hoisted out of it (which would keep it live across the whole loop and
+    // push the epilogue into spills): the empty asm hides that the lane index
+    // is loop-invariant.
+    int lane = lane0;
+    asm volatile("" : "+v"(lane));
+    // The next tile's context is rebuilt where it is needed (cheap integer
+    // work) rather than kept live across the loop.
+    const bool has_next = j + w_x < t_x;
+    const int next_lid = start + j + w_x;
+#pragma unroll
+    for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+      for (int jj = 0; jj < NTB; ++jj) acc[bb][jj] = f32x16{};
+
+    // Stage s of a tile lives in buffer s % kNBuf. Stage k + kNBuf is
+    // requested at the boundary of stage k, right after the barrier that shows
+    // every wave done with stage k's buffer and stage k + 1 landed. Requests
+    // past the tile's end go to the next tile, else re-read the last stage
+    // (a buffer nobody reads again), so every boundary issues the same loads
+    // and the wait counts stay uniform. MFMA operands are read one k-step
+    // ahead, across the stage boundary too.
+    wait_vmem<(kNBuf - 1) * LP::L>();
+    __syncthreads();
+    load_frags<NTB>(lds, 0, f[0], wv, wt, lane);
+    int k = 0;
+    // steady state: every request is a stage of this tile
+    for (; k + kNBuf < nk; ++k) {
+      unsigned char* cb = lds + (k % kNBuf) * SB;
+#pragma unroll
+      for (int s = 0; s + 1 < kSteps; ++s) {
+        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
+        mma<NTB>(f[s & 1], acc);
+      }
+      interleave<4 * NTB * (kSteps - 1), 0, (4 + NTB) * (kSteps - 1)>();
+      wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
+      stage_barrier();
+      load_stage<NTB, WT>(cb, cur.wr, cur.hr, cur.pl, wave, (k + kNBuf) * kStep);
+      load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
+      mma<NTB>(f[(kSteps - 1) & 1], acc);
+      interleave<4 * NTB, LP::L, 4 + NTB>();
+      if constexpr (SPLITK4) {
+        if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
+      }
+    }
+    // tail (at most kNBuf - 1 boundaries): requests go to the next tile's
+    // first stages, or re-read this tile's last stage when there is none
+    for (; k + 1 < nk; ++k) {
+      unsigned char* cb = lds + (k % kNBuf) * SB;
+#pragma unroll
+      for (int s = 0; s + 1 < kSteps; ++s) {
+        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
+        mma<NTB>(f[s & 1], acc);
+      }
+      wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
+      stage_barrier();
+      if (kSep && has_next) {
+        const TC nx = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
+        load_stage<NTB, WT>(cb, nx.wr, nx.hr, nx.pl, wave, (k + kNBuf - nk) * kStep);
+      } else {
+        load_stage<NTB, WT>(cb, cur.wr, cur.hr, cur.pl, wave, (nk - 1) * kStep);
+      }
+      load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
+      mma<NTB>(f[(kSteps - 1) & 1], acc);
+      if constexpr (SPLITK4) {
+        if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
+      }
+    }
+    {  // last stage: no boundary
+      const unsigned char* cb = lds + (k % kNBuf) * SB;
+#pragma unroll
+      for (int s = 0; s + 1 < kSteps; ++s) {
+        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
+        mma<NTB>(f[s & 1], acc);
+      }
+      mma<NTB>(f[(kSteps - 1) & 1], acc);
+    }
+    if constexpr (SPLITK4) {
+      quarter_fold<NTB>(acc, sum, 3);
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb)
+#pragma unroll
+        for (int jj = 0; jj < NTB; ++jj) acc[bb][jj] = sum[bb][jj];
+    }
+    if constexpr (kSep) {
+      // the last stage's buffer takes the next tile's stage kNBuf - 1
+      wait_lgkm0_vmem<63>();
+      stage_barrier();
+      if (has_next) {
+        const TC nx = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
+        load_stage<NTB, WT>(lds + ((nk - 1) % kNBuf) * SB, nx.wr, nx.hr, nx.pl, wave, (kNBuf - 1) * kStep);
+      }
+    } else {
+      wait_vmem<0>();   // every request landed: the epilogue reuses the first buffer
+      __syncthreads();
+    }
+    tile_epilogue<NTB, WT, DUMP>(a, n_vt, cur.vt, cur.v0, cur.t0, acc, scratch, wave, lane);
+    if (!has_next) break;
+    j += w_x;
+    cur = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
+    if constexpr (!kSep) {
+      __syncthreads();  // the epilogue's reads of the first buffer are done
+#pragma unroll
+      for (int s = 0; s < kNBuf; ++s)
+        load_stage<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep);
+    }
+  }
+  wait_vmem<0>();  // no global->LDS request may outlive the workgroup
+}
+
 // ---------------------------------------------------------------- merge
 
 struct MSU {
@@ -598,15 +711,32 @@ __global__ __launch_bounds__(256) void lmhead_merge_fold(const Partial* __restri
 
 int n_vocab_tiles(int V) { return (V + kVocabTile - 1) / kVocabTile; }
 
+// Compute units of the current device (cached per device).
+static int device_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  static int cache[64] = {0};
+  if (dev < 64 && cache[dev] > 0) return cache[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (dev < 64) cache[dev] = n;
+  return n;
+}
+
 template <int NTB, int WT, bool SPLITK4, bool DUMP>
-static hipError_t launch_partials_t(const LmHeadArgs& a, hipStream_t s) {
+static hipError_t launch_partials_t(const LmHeadArgs& a, bool persistent, hipStream_t s) {
   const int n_vt = n_vocab_tiles(a.V);
   constexpr int BT = Tile<NTB, WT>::BT;
   const int64_t n_tt = (a.rows + BT - 1) / BT;
   const int64_t nblk = n_tt * n_vt;
   if (nblk > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((lmhead_partials<NTB, WT, SPLITK4, DUMP>), dim3((unsigned)nblk), dim3(128 * WT), 0,
-                     s, a, n_vt);
+  int64_t grid = nblk;
+  if (persistent) {
+    const int64_t resident = (int64_t)device_cu_count() * Shape<NTB, WT, SPLITK4>::PER_CU;
+    if (resident > 0 && resident < grid) grid = resident;
+  }
+  hipLaunchKernelGGL((lmhead_partials<NTB, WT, SPLITK4, DUMP>), dim3((unsigned)grid), dim3(128 * WT), 0,
+                     s, a, n_vt, (int)n_tt);
   return hipGetLastError();
 }
 
@@ -614,20 +744,22 @@ hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, h
   const bool dump = a.logits != nullptr;
   if (splitk4) {  // a second accumulator set: at most 128 rows, 4 waves
     if (rows_per_wg >= 128)
-      return dump ? launch_partials_t<2, 2, true, true>(a, s) : launch_partials_t<2, 2, true, false>(a, s);
-    return dump ? launch_partials_t<1, 2, true, true>(a, s) : launch_partials_t<1, 2, true, false>(a, s);
+      return dump ? launch_partials_t<2, 2, true, true>(a, false, s) : launch_partials_t<2, 2, true, false>(a, false, s);
+    return dump ? launch_partials_t<1, 2, true, true>(a, false, s) : launch_partials_t<1, 2, true, false>(a, false, s);
   }
   switch (rows_per_wg) {
-    case 64: return dump ? launch_partials_t<1, 2, false, true>(a, s) : launch_partials_t<1, 2, false, false>(a, s);
-    case 128: return dump ? launch_partials_t<2, 2, false, true>(a, s) : launch_partials_t<2, 2, false, false>(a, s);
-    default:
+    case 64: return dump ? launch_partials_t<1, 2, false, true>(a, false, s) : launch_partials_t<1, 2, false, false>(a, false, s);
+    case 128: return dump ? launch_partials_t<2, 2, false, true>(a, false, s) : launch_partials_t<2, 2, false, false>(a, false, s);
+    default: {
+      const bool pers = TIM_PERSISTENT != 0;
 #if TIM_TRAIN_ROWS == 128
-      return dump ? launch_partials_t<2, 2, false, true>(a, s) : launch_partials_t<2, 2, false, false>(a, s);
+      return dump ? launch_partials_t<2, 2, false, true>(a, pers, s) : launch_partials_t<2, 2, false, false>(a, pers, s);
 #elif TIM_WIDE_WAVES
-      return dump ? launch_partials_t<2, 4, false, true>(a, s) : launch_partials_t<2, 4, false, false>(a, s);
+      return dump ? launch_partials_t<2, 4, false, true>(a, pers, s) : launch_partials_t<2, 4, false, false>(a, pers, s);
 #else
-      return dump ? launch_partials_t<4, 2, false, true>(a, s) : launch_partials_t<4, 2, false, false>(a, s);
+      return dump ? launch_partials_t<4, 2, false, true>(a, pers, s) : launch_partials_t<4, 2, false, false>(a, pers, s);
 #endif
+    }
   }
 }
 
