@@ -40,7 +40,7 @@ FLAGS = [
 
 def build(asm_dir: str | None = None, verbose: bool = False, defines=(), out: str = LIB) -> str:
     """Compile the library. `defines` are NAME=VALUE pipeline-shape overrides
-    (TIM_KSTAGE, TIM_NBUF, TIM_SWZ_SHIFT, TIM_GROUP_V); they never change results."""
+    (TIM_NBUF, TIM_GROUP_V, TIM_LOAD_AUX, TIM_PERSISTENT, TIM_WIDE_WAVES); they never change results."""
     if shutil.which(HIPCC) is None and not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     tmp = out + ".tmp"

@@ -7,27 +7,30 @@
 // among them, or on the launch grid: the batch-invariance principle of
 // Section 3.1 (fixed tiling and reduction order, no atomics).
 //
-// Kernel 1, lmhead_partials: one workgroup per (vocab tile of 256, row tile).
-//   z^T = W_tile . h_tile^T on MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulate,
-//   hidden dimension in ascending 16-element steps, one accumulation chain per
-//   logit). W is the A operand and the hidden states the B operand, so each
-//   lane's 16 accumulator registers of a 32x32 block hold 16 vocabulary entries
-//   of ONE row: most of the softmax reduction happens inside a lane.
+// Kernel 1, lmhead_partials: (vocab tile of 256, row tile) output tiles.
+//   z^T = W_tile . h_tile^T on MFMA (v_mfma_f32_16x16x32_bf16, fp32
+//   accumulate, hidden dimension in ascending 32-element steps, one
+//   accumulation chain per logit). W is the A operand and the hidden states
+//   the B operand: a lane's 4 accumulator registers of a 16x16 block hold 4
+//   consecutive vocabulary entries of ONE row. Of the two MFMA shapes with
+//   the full bf16 rate, this one moves fewer accumulator bytes per flop and
+//   sustains a higher clock under the card's power limit.
 //   Operands are staged HBM -> LDS with direct global->LDS DMA loads
-//   (global_load_lds_dwordx4), double buffered, XOR-swizzled against LDS bank
-//   conflicts. The epilogue turns the 256 logits of each row into one partial
-//   (m, s, u) = (max z, sum e^(z-m), sum e^(z-m) (z-m)) and captures the
-//   sampled token's logit from the same register value. Logits never reach HBM.
+//   (buffer_load_dwordx4 into LDS), double buffered, XOR-swizzled against LDS
+//   bank conflicts. The epilogue turns the 256 logits of each row into one
+//   partial (m, s, u) = (max z, sum e^(z-m), sum e^(z-m) (z-m)) and captures
+//   the sampled token's logit from the same register value. Logits never
+//   reach HBM.
 //
 // Kernel 2, lmhead_merge: one wavefront per row merges that row's partials with
 //   a fixed balanced binary tree over the tile index, then
 //   logp = z_tok - (M + log S) and H = log S - U / S.
 //
-// Reduction structure inside one vocab tile, for one row (fixed):
-//   lane-local: 64 values in (block b = 0..3, register r = 0..15) order;
-//   then the two lane halves (lane, lane ^ 32); then the two vocab waves.
-// The tile's max is found first (max is exact in any order), so the sums are
-// taken against the tile max directly, with no rescaling inside a tile.
+// Reduction structure inside one vocab tile, for one row (fixed): each of the
+// two vocab waves holds 128 entries of the row, 32 per lane in 4 lanes; per
+// wave, the max and then the sums against it go lane-local in (block, register)
+// order, then over the lane groups (lane ^ 16, then lane ^ 32); the two waves'
+// partials are then merged, lower vocabulary half first.
 
 #include "kernels.h"
 
@@ -35,7 +38,7 @@ namespace tim {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 // Buffer resources exist only in the device pass; the host pass compiles the
 // kernels as launch stubs and never runs their bodies.
@@ -47,21 +50,11 @@ struct rsrc_t {
 };
 #endif
 
-// Compile-time pipeline shape. None of these changes the arithmetic: the
-// hidden dimension is accumulated in the same ascending 16-element MFMA steps
-// whatever the stage depth, buffer count, LDS swizzle or tile order.
-#ifndef TIM_KSTAGE
-#define TIM_KSTAGE 64      // hidden-dimension elements per LDS stage (32 or 64)
-#endif
+// Compile-time launch and pipeline shape. None of these changes the
+// arithmetic: the hidden dimension is accumulated in the same ascending
+// 32-element MFMA steps whatever the buffer count, LDS swizzle or tile order.
 #ifndef TIM_NBUF
-#define TIM_NBUF 2         // LDS stage buffers (>= 2)
-#endif
-#ifndef TIM_SWZ_SHIFT     // LDS XOR swizzle: chunk ^= (row >> shift) & (chunks - 1); these
-#if TIM_KSTAGE == 64       // shifts make the 16 lanes of each ds_read_b128 phase hit 16
-#define TIM_SWZ_SHIFT 1    // distinct 16-byte bank groups of the 64 banks
-#else
-#define TIM_SWZ_SHIFT 2
-#endif
+#define TIM_NBUF 2         // LDS stage buffers: a power of two >= 2 (as many as fit, up to this)
 #endif
 #ifndef TIM_GROUP_V
 #define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
@@ -72,50 +65,52 @@ struct rsrc_t {
 #ifndef TIM_PERSISTENT
 #define TIM_PERSISTENT 1   // full-size launches: one workgroup per CU looping over tiles
 #endif
-#ifndef TIM_TRAIN_ROWS
-#define TIM_TRAIN_ROWS 256 // row tile of full-size launches: 256 (one workgroup per CU) or 128 (two)
-#endif
 #ifndef TIM_WIDE_WAVES
 #define TIM_WIDE_WAVES 1   // 256-row tiles: 8 waves of 128x64 (2 per SIMD); 0 = 4 waves of 128x128
 #endif
 
-constexpr int kKS = TIM_KSTAGE;
+constexpr int kKS = 64;                  // hidden-dimension elements per LDS stage
 constexpr int kRowBytes = kKS * 2;       // bytes of one row in one stage
 constexpr int kChunks = kRowBytes / 16;  // 16-byte chunks per row per stage
-constexpr int kSteps = kKS / 16;         // MFMA k-steps per stage
+constexpr int kKM = 32;                  // hidden-dimension elements per MFMA
+constexpr int kSteps = kKS / kKM;        // MFMA k-steps per stage
 constexpr int kWBytes = kVocabTile * kRowBytes;
-static_assert(kKS == 32 || kKS == 64, "stage depth");
+static_assert(kSteps == 2, "the operand double buffer alternates once per k-step");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
-// Workgroup shape: 2 waves along the vocab tile (128 entries each) times WT
-// waves along the rows, each wave holding NTB blocks of 32 rows.
+// Workgroup shape: 2 waves along the vocab tile (128 entries, 8 blocks of 16,
+// each) times WT waves along the rows, each wave holding NTB * 32 rows (2 * NTB
+// blocks of 16).
 template <int NTB, int WT>
 struct Tile {
   static constexpr int NW = 2 * WT;            // waves per workgroup
+  static constexpr int NJ = 2 * NTB;           // row blocks of 16 per wave
   static constexpr int BT = WT * NTB * 32;     // rows per workgroup
   static constexpr int kHBytes = BT * kRowBytes;
   static constexpr int kStageBytes = kWBytes + kHBytes;
 };
 
 // Residency and pipeline depth of one kernel shape. Shapes whose wave holds
-// at most 128 x 64 accumulators (and no second accumulator set) are built to
-// run two workgroups per CU -- two waves per SIMD from independent
-// workgroups, so one workgroup's barrier stalls and epilogue overlap the
-// other's MFMA stream -- and then get as many LDS stage buffers as fit in
-// half of the 160 KB LDS.
+// at most 128 x 64 accumulators (and no second accumulator set) run two
+// workgroups per CU when two stage buffers fit in half of the 160 KB LDS.
 template <int NTB, int WT, bool SPLITK4>
 struct Shape {
   using TL = Tile<NTB, WT>;
   static constexpr int PER_CU =
       (WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1;
   static constexpr int FIT = (160 * 1024 / PER_CU) / TL::kStageBytes;
-  static constexpr int NBUF = FIT < TIM_NBUF ? FIT : TIM_NBUF;
-  static_assert(NBUF >= 2, "double buffering at least");
+  static constexpr int CAP = FIT < TIM_NBUF ? FIT : TIM_NBUF;
+  // a power of two, so that it divides the stage count
+  static constexpr int NBUF = CAP >= 8 ? 8 : CAP >= 4 ? 4 : 2;
+  static_assert(FIT >= 2, "double buffering at least");
 };
 
-// 16-byte chunk c of row r sits at physical chunk c ^ swz(r) of that row.
-__device__ __forceinline__ int swz(int r) { return (r >> TIM_SWZ_SHIFT) & (kChunks - 1); }
+// 16-byte chunk c of row r sits at physical chunk c ^ swz(r) of that row. A
+// ds_read_b128 serves 16 lanes per cycle; its 16 lanes read 16 consecutive
+// rows at one logical chunk, and with 128-byte rows this swizzle puts them in
+// 16 distinct 16-byte bank groups of the 64 banks.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & (kChunks - 1); }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their maxima): at most N of
 // this wave's vector-memory loads (here: global->LDS DMA) are still in flight.
@@ -138,11 +133,14 @@ __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2
 // for what the barrier must order (its own DMA of the next stage, and its own
 // reads of the buffer about to be refilled), so no memory fence is needed;
 // the empty asm statements keep the compiler from moving memory operations
-// across it.
+// across it, and the scheduling fences keep every other instruction on its
+// side too.
 __device__ __forceinline__ void stage_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // Tile order: logical id -> (vocab tile, row tile), walking groups of
@@ -160,22 +158,21 @@ __device__ __forceinline__ void tile_of_lid(int lid, int n_vt, int n_tt, int& vt
   tt = local / gv;
 }
 
-// Per-lane byte offsets of this workgroup's DMA loads, relative to the tile's
+// Per-lane byte offsets of this wave's DMA loads, relative to the tile's
 // first row at hidden index 0. They do not change along the hidden dimension:
 // each stage only moves the scalar offset.
 template <int NTB, int WT>
 struct LoadPlan {
   static constexpr int NW = Tile<NTB, WT>::NW;
-  static constexpr int WB = 4 * kChunks / NW;                       // W blocks of 1 KB per wave
+  static constexpr int WB = 4 * kChunks / NW;                         // W blocks of 1 KB per wave
   static constexpr int HB = Tile<NTB, WT>::BT * kChunks / (64 * NW);  // hidden-state blocks per wave
-  static constexpr int L = WB + HB;                          // DMA loads per wave per stage
+  static constexpr int L = WB + HB;                                   // DMA loads per wave per stage
   uint32_t w_off[WB];
   uint32_t h_off[HB];
 };
 
 template <int NTB, int WT>
-__device__ __forceinline__ LoadPlan<NTB, WT> make_load_plan(int w_rows, int h_rows, int d, int wave,
-                                                        int lane) {
+__device__ __forceinline__ LoadPlan<NTB, WT> make_load_plan(int w_rows, int h_rows, int d, int wave, int lane) {
   LoadPlan<NTB, WT> pl;
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q) {
@@ -207,228 +204,243 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 #endif
 }
 
+// Loads [q0, q1) of one stage request (the wave's L DMA loads of a stage, W
+// blocks first), issued from scheduling unit i of nm units: load q goes with
+// unit (q - q0) * nm / (q1 - q0), so they spread evenly.
 template <int NTB, int WT>
-__device__ __forceinline__ void load_stage(unsigned char* buf, rsrc_t wr, rsrc_t hr,
-                                           const LoadPlan<NTB, WT>& pl, int wave, int soff) {
+__device__ __forceinline__ void request_part(unsigned char* buf, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl,
+                                             int wave, int soff, int q0, int q1, int i, int nm) {
 #if defined(__HIP_DEVICE_COMPILE__)
+  constexpr int WB = LoadPlan<NTB, WT>::WB;
+  constexpr int L = LoadPlan<NTB, WT>::L;
 #pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        wr, (lds_void*)(buf + (wave * LoadPlan<NTB, WT>::WB + q) * 1024), 16, pl.w_off[q], soff, 0,
-        TIM_LOAD_AUX);
-#pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        hr, (lds_void*)(buf + kWBytes + (wave * LoadPlan<NTB, WT>::HB + q) * 1024), 16, pl.h_off[q],
-        soff, 0, TIM_LOAD_AUX);
+  for (int q = 0; q < L; ++q) {
+    if (q < q0 || q >= q1 || (q - q0) * nm / (q1 - q0) != i) continue;
+    if (q < WB)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff,
+                                               0, TIM_LOAD_AUX);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWBytes + (wave * (L - WB) + (q - WB)) * 1024),
+                                               16, pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
+  }
 #endif
 }
 
-// MFMA operands of one k-step: 4 W fragments (128 vocab rows) and NTB
-// hidden-state fragments (NTB * 32 rows), 8 bf16 per lane each.
-template <int NTB>
-struct Frags {
-  bf16x8 a[4];
-  bf16x8 b[NTB];
-};
-
-template <int NTB>
-__device__ __forceinline__ void load_frags(const unsigned char* buf, int s, Frags<NTB>& f,
-                                           int wv, int wt, int lane) {
-  const int r32 = lane & 31, hi = lane >> 5;
-  const int c = ((2 * s + hi) ^ swz(r32)) * 16;  // every operand row is (multiple of 32) + r32
-#pragma unroll
-  for (int bb = 0; bb < 4; ++bb)
-    f.a[bb] = *(const bf16x8*)(buf + (wv * 128 + bb * 32 + r32) * kRowBytes + c);
-#pragma unroll
-  for (int j = 0; j < NTB; ++j)
-    f.b[j] = *(const bf16x8*)(buf + kWBytes + (wt * NTB * 32 + j * 32 + r32) * kRowBytes + c);
+// The tile's BT tokens into LDS, 64 per wave from the first BT / 64 waves
+// (rows past the batch read as 0 and are never used).
+template <int BT>
+__device__ __forceinline__ void request_tokens(int* dst, rsrc_t tr, int wave, int lane) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  if (wave < BT / 64)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(tr, (lds_void*)(dst + wave * 64), 4, (uint32_t)(wave * 64 + lane) * 4u, 0,
+                                             0, 0);
+#endif
 }
 
-// Scheduling hints for one region of the main loop: spread NV vector-memory
-// loads and ND LDS reads among the NM MFMAs (one load and one read after each
-// MFMA while they last), so that no burst of loads backs up the vector-memory
-// queue behind which a wave's next MFMA would wait.
-template <int NM, int NV, int ND>
-__device__ __forceinline__ void interleave() {
+// MFMA operands of k-step s of a stage buffer, 8 bf16 per lane: lane l reads
+// row (l % 16) of a 16-row block at hidden offset 32 s + 8 (l / 16).
+__device__ __forceinline__ bf16x8 read_operand(const unsigned char* base, int row, int s, int lane) {
+  const int c = (4 * s + (lane >> 4)) ^ swz(row);
+  return *(const bf16x8*)(base + row * kRowBytes + c * 16);
+}
+// W block bi (16 vocabulary rows) of vocab wave wv
+__device__ __forceinline__ bf16x8 read_a(const unsigned char* buf, int s, int bi, int wv, int lane) {
+  return read_operand(buf, wv * 128 + bi * 16 + (lane & 15), s, lane);
+}
+// hidden-state block bj (16 rows) of row wave wt
+template <int NTB>
+__device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj, int wt, int lane) {
+  return read_operand(buf + kWBytes, wt * NTB * 32 + bj * 16 + (lane & 15), s, lane);
+}
+
+// One k-step as 8 * NJ scheduling units, each pinned on its own: unit i
+// issues the MFMA of W block bi = i / NJ and row block bj = i % NJ (the
+// accumulation order of every logit is the k-step order; the order of the
+// units only interleaves independent chains), then its share of DMA loads
+// [q0, q1) of a stage request into `lb`, and, with READ, the reads of k-step
+// `rs` of buffer `rb`: the row-block operands into `bn` from the first units
+// on, and W block bi into `a[bi]` right after its last use here.
+template <int NTB, int WT, bool READ = true>
+__device__ __forceinline__ void kstep(bf16x8 (&a)[8], const bf16x8 (&bc)[2 * NTB], bf16x8 (&bn)[2 * NTB],
+                                      f32x4 (&acc)[8][2 * NTB], unsigned char* lb, rsrc_t wr, rsrc_t hr,
+                                      const LoadPlan<NTB, WT>& pl, int soff, int q0, int q1, const unsigned char* rb,
+                                      int rs, int wave, int wv, int wt, int lane) {
+  constexpr int NJ = 2 * NTB;
+  constexpr int NM = 8 * NJ;
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // 1 MFMA
-    if (i < NV) __builtin_amdgcn_sched_group_barrier(0x010, 1, 0);  // 1 VMEM
-    if (i < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 DS read
+    const int bi = i / NJ, bj = i % NJ;
+    acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[bi], bc[bj], acc[bi][bj], 0, 0, 0);
+    if (q1 > q0) request_part<NTB, WT>(lb, wr, hr, pl, wave, soff, q0, q1, i, NM);
+    if (READ) {
+      if (i < NJ) bn[i] = read_b<NTB>(rb, rs, i, wt, lane);
+      if (bj == NJ - 1) a[bi] = read_a(rb, rs, bi, wv, lane);
+    }
+    __builtin_amdgcn_sched_barrier(0);
   }
-}
-
-template <int NTB>
-__device__ __forceinline__ void mma(const Frags<NTB>& f, f32x16 (&acc)[4][NTB]) {
-#pragma unroll
-  for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-    for (int j = 0; j < NTB; ++j)
-      acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bb], f.b[j], acc[bb][j], 0, 0, 0);
 }
 
 // SPLITK4: after each quarter of the hidden dimension, fold the quarter's
 // accumulator into the running sum: ((q0 + q1) + q2) + q3.
 template <int NTB>
-__device__ __forceinline__ void quarter_fold(f32x16 (&acc)[4][NTB], f32x16 (&sum)[4][NTB], int q) {
+__device__ __forceinline__ void quarter_fold(f32x4 (&acc)[8][2 * NTB], f32x4 (&sum)[8][2 * NTB], int q) {
 #pragma unroll
-  for (int bb = 0; bb < 4; ++bb)
+  for (int bi = 0; bi < 8; ++bi)
 #pragma unroll
-    for (int j = 0; j < NTB; ++j) {
-      if (q == 0) sum[bb][j] = acc[bb][j];
-      else sum[bb][j] = sum[bb][j] + acc[bb][j];
-      acc[bb][j] = f32x16{};
+    for (int bj = 0; bj < 2 * NTB; ++bj) {
+      if (q == 0) sum[bi][bj] = acc[bi][bj];
+      else sum[bi][bj] = sum[bi][bj] + acc[bi][bj];
+      acc[bi][bj] = f32x4{};
     }
 }
 
-// One tile's per-row results from its accumulators (see the file comment):
-// phase A scales, masks and finds each row's tile max and gathers the token's
-// logit, phase B sums against that max, phase C combines the two vocab waves
-// and stores one Partial per row. `scratch` holds 7 * BT floats of LDS.
+struct MSU {
+  float m, s, u;
+};
+
+// (m, s, u) of the union of two disjoint vocab sets; `a` is the lower-index set.
+__device__ __forceinline__ MSU merge2(MSU a, MSU b) {
+  if (b.m == kNegInf) return a;  // empty set: exact identity
+  if (a.m == kNegInf) return b;
+  const float M = fmaxf(a.m, b.m);
+  const float da = a.m - M, db = b.m - M;
+  const float ea = exp2_hw(da * kLog2e), eb = exp2_hw(db * kLog2e);
+  MSU r;
+  r.m = M;
+  r.s = a.s * ea + b.s * eb;
+  r.u = (a.u + da * a.s) * ea + (b.u + db * b.s) * eb;
+  return r;
+}
+
+// One tile's per-row results from its accumulators. Each wave holds 128 of
+// the tile's 256 vocabulary entries of its rows: for row block bj, lane l holds
+// row (l % 16) and, in register r of W block bi, the entry
+// wv * 128 + bi * 16 + 4 (l / 16) + r. Per row block the wave takes the logits
+// z = acc * inv_tau (a multiply by exactly 1 is skipped, which changes
+// nothing), masks entries past V to -inf (tail tile only), forms its half's
+// partial (m, s, u) -- max first, then the sums against that max, lane-local
+// in (bi, r) order, then over lane ^ 16 and lane ^ 32 -- and captures the
+// sampled token's logit from the same register value. The two vocab halves
+// are merged in a fixed order (lower half first) into the tile's Partial.
+// `scratch` holds 7 * BT floats of LDS; with `tok_lds` the tile's tokens come
+// from LDS.
 template <int NTB, int WT, bool DUMP>
 __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int vt, int64_t v0, int64_t t0,
-                                              f32x16 (&acc)[4][NTB], float* scratch, int wave, int lane) {
+                                              f32x4 (&acc)[8][2 * NTB], float* scratch, const int* tok_lds, int wave,
+                                              int lane) {
   constexpr int BT = Tile<NTB, WT>::BT;
+  constexpr int NJ = 2 * NTB;
   const int wv = wave & 1, wt = wave >> 1;
   const int V = a.V;
   const int64_t rows = a.rows;
-  const int hi = lane >> 5, r32 = lane & 31;
+  const int g = lane >> 4, c16 = lane & 15;
   const float inv_tau = a.inv_tau;
-  // lane's vocab offset inside the tile for (block bb, register r):
-  //   wv*128 + bb*32 + 8*(r>>2) + 4*hi + (r&3)
-  const int64_t vlane = v0 + wv * 128 + 4 * hi;
+  const int64_t vlane = v0 + wv * 128 + 4 * g;  // + bi * 16 + r
   float* red_m = scratch;                // [2][BT]
   float* red_s = red_m + 2 * BT;         // [2][BT]
   float* red_u = red_s + 2 * BT;         // [2][BT]
   float* zt_l = red_u + 2 * BT;          // [BT]
-
-  int tok_loc[NTB];  // token - (vlane), meaningful only when the row is valid
-  bool row_ok[NTB];
-#pragma unroll
-  for (int j = 0; j < NTB; ++j) {
-    const int t_loc = wt * NTB * 32 + j * 32 + r32;
-    const int64_t tg = t0 + t_loc;
-    row_ok[j] = tg < rows;
-    const int tok = (row_ok[j] && !DUMP) ? a.tokens[tg] : -1;
-    tok_loc[j] = (tok >= 0) ? (int)((int64_t)tok - vlane) : -1000000;
-  }
-
-  // Phase A: temperature (z = acc * inv_tau, written back in place so every
-  // later use reads the same bits; a multiply by exactly 1 is skipped, which
-  // changes nothing), vocabulary mask (tail tile only: entries past V become
-  // -inf) and the row's max over the tile. Whether a tile is the tail depends
-  // only on (v0, V), so a tile takes the same path in every launch shape.
+  // Whether a tile is the tail depends only on (v0, V), so a tile takes the
+  // same path in every launch shape.
   const bool full = v0 + kVocabTile <= V;
-  if (inv_tau != 1.0f) {
+
 #pragma unroll
-    for (int j = 0; j < NTB; ++j)
+  for (int bj = 0; bj < NJ; ++bj) {
+    const int t_loc = wt * NTB * 32 + bj * 16 + c16;
+    const int64_t tg = t0 + t_loc;
+    const bool row_ok = tg < rows;
+    float z[32];  // z[4 bi + r]: entry vlane + 16 bi + r
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
+    for (int bi = 0; bi < 8; ++bi)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[bb][j][r] = acc[bb][j][r] * inv_tau;
-  }
-  if (!full) {
+      for (int r = 0; r < 4; ++r) z[bi * 4 + r] = acc[bi][bj][r];
+    if (inv_tau != 1.0f) {
 #pragma unroll
-    for (int j = 0; j < NTB; ++j)
+      for (int i = 0; i < 32; ++i) z[i] = z[i] * inv_tau;
+    }
+    if (!full) {
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (vlane + (bb * 32 + 8 * (r >> 2) + (r & 3)) >= V) acc[bb][j][r] = kNegInf;
-  }
-#pragma unroll
-  for (int j = 0; j < NTB; ++j) {
-    float mx = kNegInf;
-#pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[bb][j][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const int t_loc = wt * NTB * 32 + j * 32 + r32;
-    if (hi == 0) red_m[wv * BT + t_loc] = mx;
-    // Token gather: the row's token lies in this lane's 64 entries only for
-    // offsets tl in [0, 128) with bit 2 clear (the other lane half holds the
-    // rest). Rare, so the 64-way select runs under a divergent branch.
-    const int tl = tok_loc[j];
-    if (tl >= 0 && tl < 128 && ((tl >> 2) & 1) == 0) {
-      float zf = 0.f;
-#pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (bb * 32 + 8 * (r >> 2) + (r & 3) == tl) zf = acc[bb][j][r];
-      zt_l[t_loc] = zf;
+      for (int i = 0; i < 32; ++i)
+        if (vlane + (i >> 2) * 16 + (i & 3) >= V) z[i] = kNegInf;
     }
     if constexpr (DUMP) {
-      const int64_t tg = t0 + t_loc;
-      if (row_ok[j]) {
+      if (row_ok) {
 #pragma unroll
-        for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int64_t v = vlane + bb * 32 + 8 * (r >> 2) + (r & 3);
-            if (v < V) a.logits[tg * (int64_t)V + v] = acc[bb][j][r];
-          }
+        for (int i = 0; i < 32; ++i) {
+          const int64_t v = vlane + (i >> 2) * 16 + (i & 3);
+          if (v < V) a.logits[tg * (int64_t)V + v] = z[i];
+        }
       }
+      continue;
+    }
+    // the half's max, then e^(z - m) and e^(z - m) (z - m) summed against it;
+    // masked entries add exactly zero to both
+    float m = kNegInf;
+#pragma unroll
+    for (int i = 0; i < 32; ++i) m = fmaxf(m, z[i]);
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    float sv = 0.f, uv = 0.f;
+    if (full) {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const float x = z[i] - m;
+        const float e = exp2_hw(x * kLog2e);
+        sv = sv + e;
+        uv = __builtin_fmaf(e, x, uv);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        float x = z[i] - m;
+        float e = exp2_hw(x * kLog2e);
+        if (z[i] == kNegInf) { x = 0.f; e = 0.f; }
+        sv = sv + e;
+        uv = __builtin_fmaf(e, x, uv);
+      }
+    }
+    // lane groups: (g0 + g1, g2 + g3), then the two pairs; each step adds two
+    // values in either order, which is exact-commutative, so all four lanes agree
+    sv = sv + __shfl_xor(sv, 16);
+    uv = uv + __shfl_xor(uv, 16);
+    sv = sv + __shfl_xor(sv, 32);
+    uv = uv + __shfl_xor(uv, 32);
+    if (g == 0) {
+      red_m[wv * BT + t_loc] = m;
+      red_s[wv * BT + t_loc] = sv;
+      red_u[wv * BT + t_loc] = uv;
+    }
+    // Token gather: the lane holding the row's token has tl = token - vlane
+    // in [0, 128) with tl % 16 < 4 (entry z[4 (tl / 16) + tl % 16]). Rare, so
+    // the 32-way select runs under a divergent branch.
+    const int tok = row_ok ? (tok_lds != nullptr ? tok_lds[t_loc] : a.tokens[tg]) : -1;
+    const int tl = (tok >= 0) ? (int)((int64_t)tok - vlane) : -1000000;
+    if (tl >= 0 && tl < 128 && (tl & 15) < 4) {
+      float zf = 0.f;
+#pragma unroll
+      for (int i = 0; i < 32; ++i)
+        if ((i >> 2) * 16 + (i & 3) == tl) zf = z[i];
+      zt_l[t_loc] = zf;
     }
   }
   if constexpr (DUMP) return;
   __syncthreads();
 
-  // Phase B: s = sum e^(z - M) and u = sum e^(z - M) (z - M) against the
-  // tile max M, in fixed (bb, r) order. In the tail tile the masked entries
-  // add exactly zero to both, so valid entries see the same arithmetic as in
-  // a full tile.
+  // the tile's Partial: lower vocab half merged with the upper one
+  if (wv == 0 && g == 0) {
 #pragma unroll
-  for (int j = 0; j < NTB; ++j) {
-    const int t_loc = wt * NTB * 32 + j * 32 + r32;
-    const float M = fmaxf(red_m[t_loc], red_m[BT + t_loc]);
-    float s = 0.f, u = 0.f;
-    if (full) {
-#pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float x = acc[bb][j][r] - M;
-          const float e = exp2_hw(x * kLog2e);
-          s = s + e;
-          u = __builtin_fmaf(e, x, u);
-        }
-    } else {
-#pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float z = acc[bb][j][r];
-          float x = z - M;
-          float e = exp2_hw(x * kLog2e);
-          if (z == kNegInf) { x = 0.f; e = 0.f; }
-          s = s + e;
-          u = __builtin_fmaf(e, x, u);
-        }
-    }
-    s = s + __shfl_xor(s, 32);
-    u = u + __shfl_xor(u, 32);
-    if (hi == 0) {
-      red_s[wv * BT + t_loc] = s;
-      red_u[wv * BT + t_loc] = u;
-    }
-  }
-  __syncthreads();
-
-  // Phase C: combine the two vocab waves and store one partial per row.
-  if (wv == 0 && hi == 0) {
-#pragma unroll
-    for (int j = 0; j < NTB; ++j) {
-      const int t_loc = wt * NTB * 32 + j * 32 + r32;
+    for (int bj = 0; bj < NJ; ++bj) {
+      const int t_loc = wt * NTB * 32 + bj * 16 + c16;
       const int64_t tg = t0 + t_loc;
-      if (!row_ok[j]) continue;
+      if (tg >= rows) continue;
+      const MSU h = merge2(MSU{red_m[t_loc], red_s[t_loc], red_u[t_loc]},
+                           MSU{red_m[BT + t_loc], red_s[BT + t_loc], red_u[BT + t_loc]});
+      const int tok = tok_lds != nullptr ? tok_lds[t_loc] : a.tokens[tg];
+      const int64_t tv = (int64_t)tok - v0;
       Partial p;
-      p.m = fmaxf(red_m[t_loc], red_m[BT + t_loc]);
-      p.s = red_s[t_loc] + red_s[BT + t_loc];
-      p.u = red_u[t_loc] + red_u[BT + t_loc];
-      const int tv = tok_loc[j] + wv * 128 + 4 * hi;  // token - v0
+      p.m = h.m;
+      p.s = h.s;
+      p.u = h.u;
       p.ztok = (tv >= 0 && tv < kVocabTile) ? zt_l[t_loc] : 0.f;
       a.part[tg * n_vt + vt] = p;
     }
@@ -440,12 +452,12 @@ struct TileCtx {
   int vt;
   int64_t v0, t0;
   LoadPlan<NTB, WT> pl;
-  rsrc_t wr, hr;
+  rsrc_t wr, hr, tr;
 };
 
 template <int NTB, int WT>
-__device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int lid, int n_vt, int n_tt,
-                                                      int wave, int lane) {
+__device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int lid, int n_vt, int n_tt, int wave,
+                                                      int lane) {
   constexpr int BT = Tile<NTB, WT>::BT;
   // Opaque copies: every call recomputes its context instead of the compiler
   // reusing (and keeping live) the result of an earlier call.
@@ -461,6 +473,7 @@ __device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int l
   c.pl = make_load_plan<NTB, WT>(w_rows, h_rows, a.d, wave, lane);
   c.wr = make_rsrc((const __bf16*)a.w + c.v0 * a.d, (uint64_t)w_rows * a.d * 2);
   c.hr = make_rsrc((const __bf16*)a.hidden + c.t0 * a.d, (uint64_t)h_rows * a.d * 2);
+  c.tr = make_rsrc(a.tokens + c.t0, (uint64_t)h_rows * 4);
   return c;
 }
 
@@ -469,8 +482,18 @@ __device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int l
 // round-robin to its workgroups, so at any time the workgroups of one XCD work
 // on consecutive ids. With one workgroup per tile this is a plain launch; with
 // a grid of one workgroup per CU it is persistent, and the stage pipeline then
-// runs on across tiles: the last stage boundaries of a tile already request
-// the next tile's first stages, which land while this tile's epilogue runs.
+// runs on across tiles: the last stages of a tile already request the next
+// tile's first stages, which land while this tile's epilogue runs.
+//
+// Pipeline. Stage s of a tile (kKS hidden-dimension elements of its W and
+// hidden-state rows) lives in LDS buffer s % kNBuf. Each stage has a boundary
+// before its last k-step: every wave waits for its own reads of the stage and
+// for its own DMA of stage s + 1, then the workgroup barrier makes stage s + 1
+// visible and frees buffer s % kNBuf, which takes stage s + kNBuf, its loads
+// spread over that last k-step. MFMA operands are read one k-step ahead,
+// across the boundary too. Requests past the tile go to the next tile's
+// stages, or, with none, re-read the tile's own stages into the freed buffer,
+// so every boundary's wait counts stay the same.
 template <int NTB, int WT, bool SPLITK4, bool DUMP>
 __global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
 void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
@@ -478,14 +501,24 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
   using LP = LoadPlan<NTB, WT>;
   using TC = TileCtx<NTB, WT>;
   constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
+  static_assert((128 / kKS) % kNBuf == 0, "the stage count (a multiple of 128 / kKS) must be a multiple of kNBuf");
+  constexpr int NJ = TL::NJ;
   constexpr int BT = TL::BT;
   constexpr int SB = TL::kStageBytes;
   constexpr int EPI = 7 * BT * 4;
+  constexpr int L = LP::L;
   // Epilogue scratch of its own when it fits, so the next tile's stages can
   // land during the epilogue; otherwise it reuses the first stage buffer.
-  constexpr bool kSep = kNBuf * SB + EPI <= (160 * 1024) / Shape<NTB, WT, SPLITK4>::PER_CU;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB + (kSep ? EPI : 0)];
+  constexpr bool kSep = kNBuf * SB + EPI + (DUMP ? 0 : 2 * BT * 4) <= (160 * 1024) / Shape<NTB, WT, SPLITK4>::PER_CU;
+  // With its own scratch, the epilogue also finds the tile's tokens staged
+  // in LDS (two slots, alternating per tile), requested with the tile's first
+  // stage, so it never waits on a global load behind the next tile's stages.
+  constexpr bool kTokLds = kSep && !DUMP;
+  constexpr int TOKB = kTokLds ? 2 * BT * 4 : 0;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB + (kSep ? EPI : 0) + TOKB];
   float* scratch = (float*)(kSep ? lds + kNBuf * SB : lds);
+  int* tok_slot = (int*)(lds + kNBuf * SB + (kSep ? EPI : 0));  // [2][BT] when kTokLds
+  int par = 0;
 
   const int lane0 = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -507,13 +540,24 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
 
   TC cur = make_tile<NTB, WT>(a, start + j, n_vt, n_tt, wave, lane0);
 
+  // prologue: the tile's tokens and stages 0 .. kNBuf - 1
+  auto prologue = [&]() {
+    if constexpr (kTokLds) request_tokens<BT>(tok_slot + par * BT, cur.tr, wave, lane0);
 #pragma unroll
-  for (int s = 0; s < kNBuf; ++s)
-    load_stage<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep);
+    for (int s = 0; s < kNBuf; ++s)
+#pragma unroll
+      for (int q = 0; q < L; ++q)
+        request_part<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q, q + 1,
+                              0, 1);
+    wait_vmem<(kNBuf - 1) * L>();  // stage 0 landed
+    __syncthreads();
+  };
+  prologue();
 
-  f32x16 acc[4][NTB];
-  f32x16 sum[4][SPLITK4 ? NTB : 1];
-  Frags<NTB> f[2];
+  f32x4 acc[8][NJ];
+  f32x4 sum[8][SPLITK4 ? NJ : 1];
+  bf16x8 fa[8];      // W operands of the current k-step, refilled in place
+  bf16x8 fb[2][NJ];  // hidden-state operands, double buffered by k-step
   while (true) {
     // Per-tile lane arithmetic is recomputed inside the loop rather than
     // hoisted out of it (which would keep it live across the whole loop and
@@ -526,124 +570,82 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
     const bool has_next = j + w_x < t_x;
     const int next_lid = start + j + w_x;
 #pragma unroll
-    for (int bb = 0; bb < 4; ++bb)
+    for (int bi = 0; bi < 8; ++bi)
 #pragma unroll
-      for (int jj = 0; jj < NTB; ++jj) acc[bb][jj] = f32x16{};
+      for (int bj = 0; bj < NJ; ++bj) acc[bi][bj] = f32x4{};
 
-    // Stage s of a tile lives in buffer s % kNBuf. Stage k + kNBuf is
-    // requested at the boundary of stage k, right after the barrier that shows
-    // every wave done with stage k's buffer and stage k + 1 landed. Requests
-    // past the tile's end go to the next tile, else re-read the last stage
-    // (a buffer nobody reads again), so every boundary issues the same loads
-    // and the wait counts stay uniform. MFMA operands are read one k-step
-    // ahead, across the stage boundary too.
-    wait_vmem<(kNBuf - 1) * LP::L>();
-    __syncthreads();
-    load_frags<NTB>(lds, 0, f[0], wv, wt, lane);
+    // stage 0 has landed and is visible: after the prologue, or, when the
+    // pipeline runs on from the previous tile, since its last boundary
+#pragma unroll
+    for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = read_b<NTB>(lds, 0, bj, wt, lane);
+#pragma unroll
+    for (int bi = 0; bi < 8; ++bi) fa[bi] = read_a(lds, 0, bi, wv, lane);
     int k = 0;
     // steady state: every request is a stage of this tile
     for (; k + kNBuf < nk; ++k) {
       unsigned char* cb = lds + (k % kNBuf) * SB;
-#pragma unroll
-      for (int s = 0; s + 1 < kSteps; ++s) {
-        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
-        mma<NTB>(f[s & 1], acc);
-      }
-      interleave<4 * NTB * (kSteps - 1), 0, (4 + NTB) * (kSteps - 1)>();
-      wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
+      kstep<NTB, WT>(fa, fb[0], fb[1], acc, cb, cur.wr, cur.hr, cur.pl, 0, 0, 0, cb, 1, wave, wv, wt, lane);
+      wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      load_stage<NTB, WT>(cb, cur.wr, cur.hr, cur.pl, wave, (k + kNBuf) * kStep);
-      load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
-      mma<NTB>(f[(kSteps - 1) & 1], acc);
-      interleave<4 * NTB, LP::L, 4 + NTB>();
+      kstep<NTB, WT>(fa, fb[1], fb[0], acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep, 0, L,
+                     lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
       }
     }
-    // tail (at most kNBuf - 1 boundaries): requests go to the next tile's
-    // first stages, or re-read this tile's last stage when there is none
-    for (; k + 1 < nk; ++k) {
-      unsigned char* cb = lds + (k % kNBuf) * SB;
+    // tail: the last kNBuf stages, whose requests reach past the tile: to the
+    // next tile's first stages or, with no next tile (or no LDS to keep them
+    // through the epilogue), to this tile's own stages again. Stage k sits in
+    // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
+    {
+      const TC nx = make_tile<NTB, WT>(a, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
 #pragma unroll
-      for (int s = 0; s + 1 < kSteps; ++s) {
-        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
-        mma<NTB>(f[s & 1], acc);
+      for (int t = 0; t < kNBuf; ++t) {
+        k = nk - kNBuf + t;
+        unsigned char* cb = lds + t * SB;
+        kstep<NTB, WT>(fa, fb[0], fb[1], acc, cb, nx.wr, nx.hr, nx.pl, 0, 0, 0, cb, 1, wave, wv, wt, lane);
+        wait_lgkm0_vmem<(kNBuf - 2) * L>();
+        stage_barrier();
+        // request k + kNBuf: stage t of the next tile (with its tokens)
+        if constexpr (kTokLds) {
+          if (t == 0) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
+        }
+        if (t + 1 < kNBuf)
+          kstep<NTB, WT>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, 0, L, lds + (t + 1) * SB, 0,
+                         wave, wv, wt, lane);
+        else
+          kstep<NTB, WT, false>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, 0, L, lds, 0, wave, wv,
+                                wt, lane);
+        if constexpr (SPLITK4) {
+          if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
+        }
       }
-      wait_lgkm0_vmem<(kNBuf - 2) * LP::L>();
-      stage_barrier();
-      if (kSep && has_next) {
-        const TC nx = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
-        load_stage<NTB, WT>(cb, nx.wr, nx.hr, nx.pl, wave, (k + kNBuf - nk) * kStep);
-      } else {
-        load_stage<NTB, WT>(cb, cur.wr, cur.hr, cur.pl, wave, (nk - 1) * kStep);
-      }
-      load_frags<NTB>(lds + ((k + 1) % kNBuf) * SB, 0, f[kSteps & 1], wv, wt, lane);
-      mma<NTB>(f[(kSteps - 1) & 1], acc);
-      if constexpr (SPLITK4) {
-        if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
-      }
-    }
-    {  // last stage: no boundary
-      const unsigned char* cb = lds + (k % kNBuf) * SB;
-#pragma unroll
-      for (int s = 0; s + 1 < kSteps; ++s) {
-        load_frags<NTB>(cb, s + 1, f[(s + 1) & 1], wv, wt, lane);
-        mma<NTB>(f[s & 1], acc);
-      }
-      mma<NTB>(f[(kSteps - 1) & 1], acc);
     }
     if constexpr (SPLITK4) {
-      quarter_fold<NTB>(acc, sum, 3);
 #pragma unroll
-      for (int bb = 0; bb < 4; ++bb)
+      for (int bi = 0; bi < 8; ++bi)
 #pragma unroll
-        for (int jj = 0; jj < NTB; ++jj) acc[bb][jj] = sum[bb][jj];
+        for (int bj = 0; bj < NJ; ++bj) acc[bi][bj] = sum[bi][bj];
     }
-    if constexpr (kSep) {
-      // the last stage's buffer takes the next tile's stage kNBuf - 1
-      wait_lgkm0_vmem<63>();
-      stage_barrier();
-      if (has_next) {
-        const TC nx = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
-        load_stage<NTB, WT>(lds + ((nk - 1) % kNBuf) * SB, nx.wr, nx.hr, nx.pl, wave, (kNBuf - 1) * kStep);
-      }
-    } else {
-      wait_vmem<0>();   // every request landed: the epilogue reuses the first buffer
+    if constexpr (!kSep) {
+      wait_vmem<0>();  // every request landed: the epilogue reuses the first buffer
       __syncthreads();
     }
-    tile_epilogue<NTB, WT, DUMP>(a, n_vt, cur.vt, cur.v0, cur.t0, acc, scratch, wave, lane);
+    tile_epilogue<NTB, WT, DUMP>(a, n_vt, cur.vt, cur.v0, cur.t0, acc, scratch,
+                                 kTokLds ? tok_slot + par * BT : nullptr, wave, lane);
+    par ^= 1;
     if (!has_next) break;
     j += w_x;
     cur = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
     if constexpr (!kSep) {
       __syncthreads();  // the epilogue's reads of the first buffer are done
-#pragma unroll
-      for (int s = 0; s < kNBuf; ++s)
-        load_stage<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep);
+      prologue();
     }
   }
   wait_vmem<0>();  // no global->LDS request may outlive the workgroup
 }
 
 // ---------------------------------------------------------------- merge
-
-struct MSU {
-  float m, s, u;
-};
-
-// (m, s, u) of the union of two disjoint vocab sets; `a` is the lower-index set.
-__device__ __forceinline__ MSU merge2(MSU a, MSU b) {
-  if (b.m == kNegInf) return a;  // empty set: exact identity
-  if (a.m == kNegInf) return b;
-  const float M = fmaxf(a.m, b.m);
-  const float da = a.m - M, db = b.m - M;
-  const float ea = exp2_hw(da * kLog2e), eb = exp2_hw(db * kLog2e);
-  MSU r;
-  r.m = M;
-  r.s = a.s * ea + b.s * eb;
-  r.u = (a.u + da * a.s) * ea + (b.u + db * b.s) * eb;
-  return r;
-}
 
 __device__ __forceinline__ void finish_row(MSU v, const Partial* p, int tok, int V, int64_t row,
                                            float* logp, float* ent, float* lse) {
@@ -742,19 +744,14 @@ static hipError_t launch_partials_t(const LmHeadArgs& a, bool persistent, hipStr
 
 hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, hipStream_t s) {
   const bool dump = a.logits != nullptr;
-  if (splitk4) {  // a second accumulator set: at most 128 rows, 4 waves
-    if (rows_per_wg >= 128)
-      return dump ? launch_partials_t<2, 2, true, true>(a, false, s) : launch_partials_t<2, 2, true, false>(a, false, s);
+  if (splitk4)  // a second accumulator set: 64-row tiles of 4 waves
     return dump ? launch_partials_t<1, 2, true, true>(a, false, s) : launch_partials_t<1, 2, true, false>(a, false, s);
-  }
   switch (rows_per_wg) {
     case 64: return dump ? launch_partials_t<1, 2, false, true>(a, false, s) : launch_partials_t<1, 2, false, false>(a, false, s);
     case 128: return dump ? launch_partials_t<2, 2, false, true>(a, false, s) : launch_partials_t<2, 2, false, false>(a, false, s);
     default: {
       const bool pers = TIM_PERSISTENT != 0;
-#if TIM_TRAIN_ROWS == 128
-      return dump ? launch_partials_t<2, 2, false, true>(a, pers, s) : launch_partials_t<2, 2, false, false>(a, pers, s);
-#elif TIM_WIDE_WAVES
+#if TIM_WIDE_WAVES
       return dump ? launch_partials_t<2, 4, false, true>(a, pers, s) : launch_partials_t<2, 4, false, false>(a, pers, s);
 #else
       return dump ? launch_partials_t<4, 2, false, true>(a, pers, s) : launch_partials_t<4, 2, false, false>(a, pers, s);

@@ -23,7 +23,7 @@ inline float inv_temperature(float temperature) {
 inline int row_tile_for(int64_t rows, int32_t mode, bool splitk4) {
   int rt = 256;
   if (mode == TIM_MODE_ROLLOUT) rt = rows <= 64 ? 64 : (rows <= 128 ? 128 : 256);
-  if (splitk4 && rt > 128) rt = 128;  // the split-K engine keeps a second accumulator set
+  if (splitk4) rt = 64;  // the split-K engine keeps a second accumulator set
   return rt;
 }
 
