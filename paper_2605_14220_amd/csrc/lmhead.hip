@@ -129,6 +129,23 @@ __device__ __forceinline__ void wait_lgkm0_vmem() {
 
 __device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Combine a value over the four lane groups (lanes l, l ^ 16, l ^ 32, l ^ 48)
+// as (g0 op g1) op (g2 op g3). v_permlane16_swap / v_permlane32_swap of a
+// register with itself return, in every lane, the two halves' values in the
+// same order, so every lane computes the same operation on the same operands.
+__device__ __forceinline__ float group_sum(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+__device__ __forceinline__ float group_max(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+
 // Workgroup barrier between pipeline stages. Each wave has already waited
 // for what the barrier must order (its own DMA of the next stage, and its own
 // reads of the buffer about to be refilled), so no memory fence is needed;
@@ -141,7 +158,17 @@ __device__ __forceinline__ void stage_barrier() {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   __builtin_amdgcn_sched_barrier(0);
+  // the k-step after a boundary runs at raised priority (see region_a_prio)
+  __builtin_amdgcn_s_setprio(1);
 }
+
+// Wave priority of the k-step before a boundary. The two waves sharing a SIMD
+// drift apart (the older one issues first); a wave that is already into the
+// next stage's first k-step yields to its sibling still finishing the k-step
+// after the last boundary, so the two reach the next barrier closer together
+// and the time one of them idles there -- with the other issuing MFMAs alone,
+// which does not fill the pipe -- shrinks.
+__device__ __forceinline__ void region_a_prio() { __builtin_amdgcn_s_setprio(0); }
 
 // Tile order: logical id -> (vocab tile, row tile), walking groups of
 // TIM_GROUP_V vocab tiles with the row tiles outer and the vocab tiles inner,
@@ -204,25 +231,19 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 #endif
 }
 
-// Loads [q0, q1) of one stage request (the wave's L DMA loads of a stage, W
-// blocks first), issued from scheduling unit i of nm units: load q goes with
-// unit (q - q0) * nm / (q1 - q0), so they spread evenly.
+// Load q of a stage request: the wave's L DMA loads of a stage, W blocks first.
 template <int NTB, int WT>
-__device__ __forceinline__ void request_part(unsigned char* buf, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl,
-                                             int wave, int soff, int q0, int q1, int i, int nm) {
+__device__ __forceinline__ void request_load(unsigned char* buf, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl,
+                                             int wave, int soff, int q) {
 #if defined(__HIP_DEVICE_COMPILE__)
   constexpr int WB = LoadPlan<NTB, WT>::WB;
   constexpr int L = LoadPlan<NTB, WT>::L;
-#pragma unroll
-  for (int q = 0; q < L; ++q) {
-    if (q < q0 || q >= q1 || (q - q0) * nm / (q1 - q0) != i) continue;
-    if (q < WB)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff,
-                                               0, TIM_LOAD_AUX);
-    else
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWBytes + (wave * (L - WB) + (q - WB)) * 1024),
-                                               16, pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
-  }
+  if (q < WB)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff, 0,
+                                             TIM_LOAD_AUX);
+  else
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWBytes + (wave * (L - WB) + (q - WB)) * 1024), 16,
+                                             pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
 #endif
 }
 
@@ -260,18 +281,23 @@ __device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj
 // [q0, q1) of a stage request into `lb`, and, with READ, the reads of k-step
 // `rs` of buffer `rb`: the row-block operands into `bn` from the first units
 // on, and W block bi into `a[bi]` right after its last use here.
-template <int NTB, int WT, bool READ = true>
+template <int NTB, int WT, bool LOAD, bool READ = true>
 __device__ __forceinline__ void kstep(bf16x8 (&a)[8], const bf16x8 (&bc)[2 * NTB], bf16x8 (&bn)[2 * NTB],
                                       f32x4 (&acc)[8][2 * NTB], unsigned char* lb, rsrc_t wr, rsrc_t hr,
-                                      const LoadPlan<NTB, WT>& pl, int soff, int q0, int q1, const unsigned char* rb,
-                                      int rs, int wave, int wv, int wt, int lane) {
+                                      const LoadPlan<NTB, WT>& pl, int soff, const unsigned char* rb, int rs, int wave,
+                                      int wv, int wt, int lane) {
   constexpr int NJ = 2 * NTB;
   constexpr int NM = 8 * NJ;
+  constexpr int L = LoadPlan<NTB, WT>::L;
+  static_assert(L <= NM, "at most one DMA load per unit");
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     const int bi = i / NJ, bj = i % NJ;
     acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[bi], bc[bj], acc[bi][bj], 0, 0, 0);
-    if (q1 > q0) request_part<NTB, WT>(lb, wr, hr, pl, wave, soff, q0, q1, i, NM);
+    if (LOAD) {  // load q goes with unit q * NM / L
+      const int q = (i * L + NM - 1) / NM;
+      if (q < L && q * NM / L == i) request_load<NTB, WT>(lb, wr, hr, pl, wave, soff, q);
+    }
     if (READ) {
       if (i < NJ) bn[i] = read_b<NTB>(rb, rs, i, wt, lane);
       if (bj == NJ - 1) a[bi] = read_a(rb, rs, bi, wv, lane);
@@ -373,13 +399,15 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
       }
       continue;
     }
-    // the half's max, then e^(z - m) and e^(z - m) (z - m) summed against it;
-    // masked entries add exactly zero to both
+    // the half's max, then e^(z - m) and e^(z - m) (z - m) summed against it
+    // (z - m is exact 0 at the max, which so adds exactly 1 and 0); masked
+    // entries add exactly zero to both. Lane groups combine as
+    // (g0 + g1) + (g2 + g3): each permlane swap leaves one operand pair in the
+    // same order in all four lanes, so they agree bit for bit.
     float m = kNegInf;
 #pragma unroll
     for (int i = 0; i < 32; ++i) m = fmaxf(m, z[i]);
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
+    m = group_max(m);
     float sv = 0.f, uv = 0.f;
     if (full) {
 #pragma unroll
@@ -399,12 +427,8 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
         uv = __builtin_fmaf(e, x, uv);
       }
     }
-    // lane groups: (g0 + g1, g2 + g3), then the two pairs; each step adds two
-    // values in either order, which is exact-commutative, so all four lanes agree
-    sv = sv + __shfl_xor(sv, 16);
-    uv = uv + __shfl_xor(uv, 16);
-    sv = sv + __shfl_xor(sv, 32);
-    uv = uv + __shfl_xor(uv, 32);
+    sv = group_sum(sv);
+    uv = group_sum(uv);
     if (g == 0) {
       red_m[wv * BT + t_loc] = m;
       red_s[wv * BT + t_loc] = sv;
@@ -547,8 +571,7 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
     for (int s = 0; s < kNBuf; ++s)
 #pragma unroll
       for (int q = 0; q < L; ++q)
-        request_part<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q, q + 1,
-                              0, 1);
+        request_load<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q);
     wait_vmem<(kNBuf - 1) * L>();  // stage 0 landed
     __syncthreads();
   };
@@ -584,11 +607,12 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
     // steady state: every request is a stage of this tile
     for (; k + kNBuf < nk; ++k) {
       unsigned char* cb = lds + (k % kNBuf) * SB;
-      kstep<NTB, WT>(fa, fb[0], fb[1], acc, cb, cur.wr, cur.hr, cur.pl, 0, 0, 0, cb, 1, wave, wv, wt, lane);
+      region_a_prio();
+      kstep<NTB, WT, false>(fa, fb[0], fb[1], acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
       wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      kstep<NTB, WT>(fa, fb[1], fb[0], acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep, 0, L,
-                     lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
+      kstep<NTB, WT, true>(fa, fb[1], fb[0], acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
+                           lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
       }
@@ -603,7 +627,8 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
       for (int t = 0; t < kNBuf; ++t) {
         k = nk - kNBuf + t;
         unsigned char* cb = lds + t * SB;
-        kstep<NTB, WT>(fa, fb[0], fb[1], acc, cb, nx.wr, nx.hr, nx.pl, 0, 0, 0, cb, 1, wave, wv, wt, lane);
+        region_a_prio();
+        kstep<NTB, WT, false>(fa, fb[0], fb[1], acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
         wait_lgkm0_vmem<(kNBuf - 2) * L>();
         stage_barrier();
         // request k + kNBuf: stage t of the next tile (with its tokens)
@@ -611,11 +636,11 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
           if (t == 0) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
         }
         if (t + 1 < kNBuf)
-          kstep<NTB, WT>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, 0, L, lds + (t + 1) * SB, 0,
-                         wave, wv, wt, lane);
+          kstep<NTB, WT, true>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
+                               wave, wv, wt, lane);
         else
-          kstep<NTB, WT, false>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, 0, L, lds, 0, wave, wv,
-                                wt, lane);
+          kstep<NTB, WT, true, false>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
+                                      wt, lane);
         if constexpr (SPLITK4) {
           if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
         }
