@@ -277,30 +277,45 @@ __device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj
 // One k-step as 8 * NJ scheduling units, each pinned on its own: unit i
 // issues the MFMA of W block bi = i / NJ and row block bj = i % NJ (the
 // accumulation order of every logit is the k-step order; the order of the
-// units only interleaves independent chains), then its share of DMA loads
-// [q0, q1) of a stage request into `lb`, and, with READ, the reads of k-step
-// `rs` of buffer `rb`: the row-block operands into `bn` from the first units
-// on, and W block bi into `a[bi]` right after its last use here.
-template <int NTB, int WT, bool LOAD, bool READ = true>
-__device__ __forceinline__ void kstep(bf16x8 (&a)[8], const bf16x8 (&bc)[2 * NTB], bf16x8 (&bn)[2 * NTB],
-                                      f32x4 (&acc)[8][2 * NTB], unsigned char* lb, rsrc_t wr, rsrc_t hr,
-                                      const LoadPlan<NTB, WT>& pl, int soff, const unsigned char* rb, int rs, int wave,
-                                      int wv, int wt, int lane) {
+// units only interleaves independent chains), then, with LOAD, its share of
+// the DMA loads of a stage request into `lb`, and, with READ, the reads of
+// k-step `rs` of buffer `rb`. Operands alternate between two register sets by
+// k-step parity P: the row-block operands always, read from the first units
+// on; the W operands too with AD (then read right after the row blocks, so
+// every read lands early), else the single W set is refilled block by block
+// right after each block's last use here.
+template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true>
+__device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
+                                      unsigned char* lb, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl, int soff,
+                                      const unsigned char* rb, int rs, int wave, int wv, int wt, int lane) {
   constexpr int NJ = 2 * NTB;
   constexpr int NM = 8 * NJ;
   constexpr int L = LoadPlan<NTB, WT>::L;
+  constexpr int PA = AD ? P : 0, PN = AD ? (P ^ 1) : 0;
   static_assert(L <= NM, "at most one DMA load per unit");
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     const int bi = i / NJ, bj = i % NJ;
-    acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[bi], bc[bj], acc[bi][bj], 0, 0, 0);
+    acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[PA][bi], fb[P][bj], acc[bi][bj], 0, 0, 0);
     if (LOAD) {  // load q goes with unit q * NM / L
       const int q = (i * L + NM - 1) / NM;
       if (q < L && q * NM / L == i) request_load<NTB, WT>(lb, wr, hr, pl, wave, soff, q);
     }
     if (READ) {
-      if (i < NJ) bn[i] = read_b<NTB>(rb, rs, i, wt, lane);
-      if (bj == NJ - 1) a[bi] = read_a(rb, rs, bi, wv, lane);
+      if (!AD && i < NJ) fb[P ^ 1][i] = read_b<NTB>(rb, rs, i, wt, lane);
+      if (AD) {
+        // NJ + 8 reads spread evenly over the units, in the order the next
+        // k-step consumes them: a0, b0 .. b[NJ-1], a1 .. a7
+        constexpr int NR = NJ + 8;
+        const int r = (i * NR + NM - 1) / NM;
+        if (r < NR && r * NM / NR == i) {
+          if (r == 0) fa[PN][0] = read_a(rb, rs, 0, wv, lane);
+          else if (r <= NJ) fb[P ^ 1][r - 1] = read_b<NTB>(rb, rs, r - 1, wt, lane);
+          else fa[PN][r - NJ] = read_a(rb, rs, r - NJ, wv, lane);
+        }
+      } else {
+        if (bj == NJ - 1) fa[PN][bi] = read_a(rb, rs, bi, wv, lane);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -579,8 +594,10 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
 
   f32x4 acc[8][NJ];
   f32x4 sum[8][SPLITK4 ? NJ : 1];
-  bf16x8 fa[8];      // W operands of the current k-step, refilled in place
-  bf16x8 fb[2][NJ];  // hidden-state operands, double buffered by k-step
+  // One wave per SIMD (four waves) leaves registers for a second W operand set.
+  constexpr bool kAD = TL::NW == 4 && Shape<NTB, WT, SPLITK4>::PER_CU == 1;
+  bf16x8 fa[2][8];   // W operands by k-step parity (with kAD), else fa[0] refilled in place
+  bf16x8 fb[2][NJ];  // hidden-state operands, double buffered by k-step parity
   while (true) {
     // Per-tile lane arithmetic is recomputed inside the loop rather than
     // hoisted out of it (which would keep it live across the whole loop and
@@ -602,17 +619,17 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
 #pragma unroll
     for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = read_b<NTB>(lds, 0, bj, wt, lane);
 #pragma unroll
-    for (int bi = 0; bi < 8; ++bi) fa[bi] = read_a(lds, 0, bi, wv, lane);
+    for (int bi = 0; bi < 8; ++bi) fa[0][bi] = read_a(lds, 0, bi, wv, lane);
     int k = 0;
     // steady state: every request is a stage of this tile
     for (; k + kNBuf < nk; ++k) {
       unsigned char* cb = lds + (k % kNBuf) * SB;
       region_a_prio();
-      kstep<NTB, WT, false>(fa, fb[0], fb[1], acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
+      kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
       wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      kstep<NTB, WT, true>(fa, fb[1], fb[0], acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
-                           lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
+      kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
+                                   lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
       }
@@ -628,7 +645,7 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
         k = nk - kNBuf + t;
         unsigned char* cb = lds + t * SB;
         region_a_prio();
-        kstep<NTB, WT, false>(fa, fb[0], fb[1], acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
+        kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
         wait_lgkm0_vmem<(kNBuf - 2) * L>();
         stage_barrier();
         // request k + kNBuf: stage t of the next tile (with its tokens)
@@ -636,11 +653,11 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
           if (t == 0) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
         }
         if (t + 1 < kNBuf)
-          kstep<NTB, WT, true>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
-                               wave, wv, wt, lane);
+          kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
+                                       wave, wv, wt, lane);
         else
-          kstep<NTB, WT, true, false>(fa, fb[1], fb[0], acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
-                                      wt, lane);
+          kstep<NTB, WT, 1, kAD, true, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
+                                              wt, lane);
         if constexpr (SPLITK4) {
           if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
         }
