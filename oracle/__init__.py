@@ -10,7 +10,8 @@ Parity status (each function's own docstring names its pins):
 
 * ``logprobs``      pinned (closed forms, brute force, library routines).
 * ``mismatch``      pinned (Table 1 of the paper, closed forms, series).
+* ``mismatch_seq``  pinned (closed forms, telescoping, brute force, boundaries).
 """
 
 from .logprobs import bf16_to_f64, logits, logprobs  # noqa: F401
-from .mismatch import mismatch  # noqa: F401
+from .mismatch import mismatch, mismatch_seq  # noqa: F401

@@ -301,3 +301,101 @@ def test_truncated_weight():
     assert 0 < w[4] < 1e-21
     _, _, wc = oracle.mismatch(np.array([0.0, math.log(0.5) + 1e-9]), np.zeros(2), 0.5)
     assert wc[0] == 0.5 and wc[1] == 0.5
+
+
+# ---------------------------------------------------------------- sequence level (Section 4.2, appendix)
+
+def _random_stream(seed, n_resp, max_len, scale=1e-2):
+    rng = np.random.default_rng(seed)
+    lens = rng.integers(0, max_len + 1, size=n_resp)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    T = int(cu[-1])
+    b = (rng.standard_normal(T) - 2.0).astype(np.float32)
+    a = (b + scale * rng.standard_normal(T)).astype(np.float32)
+    return a, b, cu
+
+
+@pytest.mark.parametrize("est", ["k1", "k3"])
+def test_seq_constant_delta_closed_form(est):
+    """A response of L tokens with the same delta scores L * K(delta) (exactly,
+    as math.fsum of equal terms is the correctly rounded product)."""
+    for delta, L in [(-0.133, 7), (0.01, 1000), (1e-4, 16384), (0.5, 3)]:
+        a = np.full(L, delta, dtype=np.float64)
+        score, _, _ = oracle.mismatch_seq(a, np.zeros(L), [0, L], est, 2.0, 1e-3)
+        K = -delta if est == "k1" else math.expm1(delta) - delta
+        assert score[0] == L * K, (est, delta, L)
+
+
+def test_seq_k1_telescopes():
+    """K1 = -log r_corr = logp_b - logp_a, so a response's K1 score is
+    sum(logp_b) - sum(logp_a) over it."""
+    a, b, cu = _random_stream(3, 20, 300)
+    score, _, _ = oracle.mismatch_seq(a, b, cu, "k1", 2.0, 1e-3)
+    for j in range(len(cu) - 1):
+        s0, s1 = cu[j], cu[j + 1]
+        ref = math.fsum(b[s0:s1].astype(np.float64)) - math.fsum(a[s0:s1].astype(np.float64))
+        assert abs(score[j] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+@pytest.mark.parametrize("C,tau", [(2.0, 1e-3), (0.5, 0.0), (2.0, -1.0)])
+def test_seq_identical_inputs(C, tau):
+    x = (np.random.default_rng(4).standard_normal(50) - 3).astype(np.float32)
+    cu = np.array([0, 10, 10, 50], dtype=np.int64)
+    for est in ("k1", "k3"):
+        score, keep, w = oracle.mismatch_seq(x, x, cu, est, C, tau)
+        assert (score == 0).all()
+        assert (keep == (0.0 <= tau)).all()
+        assert (w == (min(1.0, C) if 0.0 <= tau else 0.0)).all()
+
+
+def test_seq_empty_responses_and_keep_boundary():
+    a = np.array([0.1, -0.2, 0.05], dtype=np.float64)
+    b = np.zeros(3)
+    cu = np.array([0, 0, 3, 3], dtype=np.int64)
+    score, keep, w = oracle.mismatch_seq(a, b, cu, "k3", 2.0, 1e-3)
+    assert score[0] == 0 and score[2] == 0 and keep[0] and keep[2]
+    s = score[1]
+    assert s > 0
+    # keep is score <= tau: the score itself is kept, the next float below rejects
+    _, keep_eq, w_eq = oracle.mismatch_seq(a, b, cu, "k3", 2.0, s)
+    _, keep_lt, w_lt = oracle.mismatch_seq(a, b, cu, "k3", 2.0, np.nextafter(s, -np.inf))
+    assert keep_eq[1] and not keep_lt[1]
+    np.testing.assert_allclose(w_eq, np.minimum(np.exp(a - b), 2.0), rtol=1e-15)
+    assert (w_lt == 0).all()
+
+
+@pytest.mark.parametrize("est", ["k1", "k3"])
+def test_seq_brute_force(est):
+    """Token-by-token accumulation in plain Python (each token looks up its
+    response by scanning the offsets) on small random streams."""
+    a, b, cu = _random_stream(11, 13, 40, scale=0.05)
+    C, tau = 1.5, 2e-3
+    score, keep, w = oracle.mismatch_seq(a, b, cu, est, C, tau)
+    n = len(cu) - 1
+    acc = [0.0] * n
+    for t in range(len(a)):
+        j = next(j for j in range(n) if cu[j] <= t < cu[j + 1])
+        d = float(a[t]) - float(b[t])
+        acc[j] += (-d) if est == "k1" else (math.exp(d) - 1.0 - d)
+    for j in range(n):
+        assert abs(score[j] - acc[j]) <= 1e-12 + 1e-9 * abs(acc[j])
+        assert keep[j] == (score[j] <= tau)
+        for t in range(cu[j], cu[j + 1]):
+            d = float(a[t]) - float(b[t])
+            ref = min(math.exp(d), C) if keep[j] else 0.0
+            assert abs(w[t] - ref) <= 4e-16 * ref
+    if est == "k3":
+        assert (score >= 0).all()
+    assert 0 < keep.sum() < n  # the draw exercises both outcomes
+
+
+def test_seq_response_order_is_irrelevant():
+    a, b, cu = _random_stream(5, 9, 60)
+    score, keep, w = oracle.mismatch_seq(a, b, cu, "k3", 2.0, 1e-3)
+    perm = np.random.default_rng(6).permutation(len(cu) - 1)
+    pieces = [(a[cu[j]:cu[j + 1]], b[cu[j]:cu[j + 1]]) for j in perm]
+    a2 = np.concatenate([p[0] for p in pieces])
+    b2 = np.concatenate([p[1] for p in pieces])
+    cu2 = np.concatenate([[0], np.cumsum([len(p[0]) for p in pieces])])
+    score2, keep2, _ = oracle.mismatch_seq(a2, b2, cu2, "k3", 2.0, 1e-3)
+    assert (score2 == score[perm]).all() and (keep2 == keep[perm]).all()

@@ -29,6 +29,11 @@ MUTATIONS = [
     ("mismatch.py", "k3 = np.expm1(delta) - delta", "k3 = np.exp(delta) - delta"),
     ("mismatch.py", "w = np.minimum(np.exp(delta), float(C))", "w = np.maximum(np.exp(delta), float(C))"),
     ("mismatch.py", "w = np.minimum(np.exp(delta), float(C))", "w = np.minimum(np.exp(-delta), float(C))"),
+    ("mismatch.py", "per_token = -delta if", "per_token = delta if"),
+    ("mismatch.py", "score[j] = math.fsum(per_token[s0:s1].tolist())", "score[j] = math.fsum(per_token[s0:s1 + 1].tolist())"),
+    ("mismatch.py", "keep[j] = bool(score[j] <= tau_seq)", "keep[j] = bool(score[j] < tau_seq)"),
+    ("mismatch.py", "        if keep[j]:\n", "        if True:\n"),
+    ("mismatch.py", "else np.expm1(delta) - delta\n", "else np.expm1(delta) + delta\n"),
 ]
 
 
