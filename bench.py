@@ -227,6 +227,31 @@ def main(argv=None):
         del src, dst
         log("[bench] calibration copy: 3 x torch.neg over 2^28 fp32 (1 GiB in, 1 GiB out)")
 
+    # sequence level (Section 4.2): K3 scores of the packed responses, the
+    # rejection mask at tau_seq = 0.001 and the truncated-and-rejected weights
+    lens = cfg.lengths()
+    cu = torch.as_tensor(np.concatenate([[0], np.cumsum(lens)]).astype(np.int64), device=dev)
+    seq_out = (torch.empty(len(lens), dtype=torch.float64, device=dev),
+               torch.empty(len(lens), dtype=torch.uint8, device=dev), torch.empty(T, dtype=torch.float32, device=dev))
+    for _ in range(3):
+        tim.mismatch_seq(logp, logp_b, cu, C=2.0, tau_seq=1e-3, out=seq_out)
+    q0 = torch.cuda.Event(enable_timing=True)
+    q1 = torch.cuda.Event(enable_timing=True)
+    n_seq_calls = 50
+    torch.cuda.synchronize()
+    q0.record(stream)
+    for _ in range(n_seq_calls):
+        tim.mismatch_seq(logp, logp_b, cu, C=2.0, tau_seq=1e-3, out=seq_out)
+    q1.record(stream)
+    torch.cuda.synchronize()
+    seq_ms = q0.elapsed_time(q1) / n_seq_calls
+    seq_bytes = 12.0 * T + 9.0 * len(lens)
+    seq = {"responses": len(lens), "tokens": T, "ms_per_call": seq_ms, "tokens_per_s": T / (seq_ms / 1e3),
+           "achieved_GBps": seq_bytes / (seq_ms / 1e3) / 1e9, "bytes_per_call": seq_bytes,
+           "rejected_at_tau_1e-3": int((seq_out[1] == 0).sum().item()),
+           "max_k3_score": float(seq_out[0].max().item())}
+    log(f"[bench] sequence-level K3 scores / mask / weights over {len(lens)} responses: {seq_ms * 1e3:.1f} us/call")
+
     # mismatch report between the two engines (context)
     dl = stats[0].abs()
     q = torch.quantile(dl.float(), torch.tensor([0.5, 0.99], device=dev)).tolist()
@@ -274,6 +299,7 @@ def main(argv=None):
         "parity_sample": parity,
         "mismatch_vs_splitk4": mis,
         "rollout_decode": rollout,
+        "sequence_mismatch": seq,
     }
     print(json.dumps(out), flush=True)
 

@@ -142,6 +142,50 @@ tim_status tim_logprobs_merge(const void* workspace, const int32_t* tokens, int6
 tim_status tim_mismatch(const float* logp_a, const float* logp_b, int64_t T, float C,
                         float* log_ratio, float* k3, float* is_weight, hipStream_t stream);
 
+/* Estimator of the sequence-level score (Section 4.1): K1(r) = -log r,
+ * K3(r) = (r - 1) - log r. */
+typedef enum {
+  TIM_EST_K1 = 1,
+  TIM_EST_K3 = 3
+} tim_estimator;
+
+/* Sequence-level mismatch score, rejection mask and token weights
+ * (Section 4.2: token-level truncation min(r_corr, tau_tok) and sequence-level
+ * rejection 1[S_seq <= tau_seq] with S_seq = sum over the response of
+ * K(r_corr,t); the appendix's tis-srs-k1/k3-corr objectives weight each token's
+ * PPO term by both).
+ *
+ * The stream of T tokens packs n_seq responses: response j is the tokens
+ * [cu_seqlens[j], cu_seqlens[j+1]). With delta_t = logp_a[t] - logp_b[t]
+ * (a = trainer, b = rollout, as in tim_mismatch) and r_corr = exp(delta):
+ *   score[j]  = sum over response j of K(delta_t), K1 = -delta,
+ *               K3 = expm1(delta) - delta; delta and the sum are fp64, summed in
+ *               a fixed order that depends only on the response's length (a
+ *               response's score is bitwise the same wherever it sits);
+ *   keep[j]   = 1 if score[j] <= tau_seq, else 0 (a NaN score rejects);
+ *   weight[t] = keep[j] ? min(exp(delta_t), C) : 0 for t in response j, in
+ *               fp32 (tim_mismatch's is_weight, zeroed in rejected responses).
+ *
+ * cu_seqlens  int64 [n_seq + 1] DEVICE array: non-decreasing, cu_seqlens[0] = 0,
+ *             cu_seqlens[n_seq] = T. It is only read on the device: bounds are
+ *             clamped into [0, T] and reversed bounds give an empty response
+ *             (score 0), so malformed offsets cannot make the kernel touch
+ *             memory outside the arrays (overlapping responses are not
+ *             detected; their weights are then unspecified).
+ * estimator   TIM_EST_K1 or TIM_EST_K3.
+ * C           finite and > 0 (tau_tok; 2 in the paper); tau_seq must not be NaN
+ *             (0.001 in the paper).
+ * score fp64 [n_seq], keep uint8 [n_seq], weight fp32 [T]: device outputs, any
+ *             may be NULL (not written). Tokens outside every response are not
+ *             written.
+ * n_seq == 0 is a no-op. Errors: TIM_ERR_SHAPE for T < 0, n_seq < 0 or
+ * n_seq > 2^31 - 1; TIM_ERR_NULL for NULL cu_seqlens, or NULL logp_a / logp_b
+ * with T > 0; TIM_ERR_VALUE for an unknown estimator, a bad C or a NaN tau_seq. */
+tim_status tim_mismatch_seq(const float* logp_a, const float* logp_b, int64_t T,
+                            const int64_t* cu_seqlens, int64_t n_seq, int32_t estimator,
+                            float C, double tau_seq,
+                            double* score, uint8_t* keep, float* weight, hipStream_t stream);
+
 /* Test and debugging aid: writes the fp32 logits z[T, V] (row-major) exactly as
  * tim_logprobs forms them before the softmax (same kernel code, same
  * accumulation order, same temperature multiply), for checking the gather and

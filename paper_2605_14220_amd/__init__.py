@@ -41,6 +41,11 @@ class Order(enum.IntEnum):
     SPLITK4 = 1
 
 
+class Estimator(enum.IntEnum):
+    K1 = 1
+    K3 = 3
+
+
 class TimError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{msg} (status {status})")
@@ -75,6 +80,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tim_mismatch.restype = c.c_int
     lib.tim_mismatch.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_float, c.c_void_p, c.c_void_p,
                                  c.c_void_p, c.c_void_p]
+    lib.tim_mismatch_seq.restype = c.c_int
+    lib.tim_mismatch_seq.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int32,
+                                     c.c_float, c.c_double, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p]
     lib.tim_logits.restype = c.c_int
     lib.tim_logits.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32, c.c_float,
                                c.c_int32, c.c_void_p, c.c_void_p]
@@ -192,6 +200,32 @@ def mismatch(logp_a: torch.Tensor, logp_b: torch.Tensor, C: float = 2.0, out: tu
     _require_gpu(*out)
     _check(lib.tim_mismatch(_ptr(logp_a), _ptr(logp_b), T, float(C), _ptr(out[0]), _ptr(out[1]),
                             _ptr(out[2]), _stream(logp_a.device)))
+    return out
+
+
+def mismatch_seq(logp_a: torch.Tensor, logp_b: torch.Tensor, cu_seqlens: torch.Tensor, C: float = 2.0,
+                 tau_seq: float = 1e-3, estimator: Estimator = Estimator.K3, out: tuple | None = None):
+    """Per-response mismatch score, keep mask and per-token weights of a packed stream.
+
+    logp_a (trainer) and logp_b (rollout) fp32 [T]; cu_seqlens int64 [n + 1] offsets of the
+    n responses. Returns (score fp64 [n], keep uint8 [n], weight fp32 [T]) with
+    score = sum_t K(delta_t) (K1 = -delta, K3 = expm1(delta) - delta), keep = score <= tau_seq,
+    weight = keep * min(exp(delta), C). See include/tim.h."""
+    lib = load_library()
+    if logp_a.dtype != torch.float32 or logp_b.dtype != torch.float32 or logp_a.shape != logp_b.shape:
+        raise TypeError("tim.mismatch_seq: logp_a and logp_b must be fp32 of one shape")
+    if cu_seqlens.dtype != torch.int64 or cu_seqlens.dim() != 1 or cu_seqlens.numel() < 1:
+        raise TypeError("tim.mismatch_seq: cu_seqlens must be a non-empty int64 vector")
+    _require_gpu(logp_a, logp_b, cu_seqlens)
+    T = logp_a.numel()
+    n = cu_seqlens.numel() - 1
+    dev = logp_a.device
+    if out is None:
+        out = (torch.empty(n, dtype=torch.float64, device=dev), torch.empty(n, dtype=torch.uint8, device=dev),
+               torch.zeros(T, dtype=torch.float32, device=dev))
+    _require_gpu(*out)
+    _check(lib.tim_mismatch_seq(_ptr(logp_a), _ptr(logp_b), T, _ptr(cu_seqlens), n, int(estimator), float(C),
+                                float(tau_seq), _ptr(out[0]), _ptr(out[1]), _ptr(out[2]), _stream(dev)))
     return out
 
 

@@ -39,5 +39,10 @@ hipError_t launch_merge(const Partial* part, const int32_t* tokens, int64_t rows
                         bool left_fold, float* logp, float* entropy, float* lse, hipStream_t s);
 hipError_t launch_mismatch(const float* a, const float* b, int64_t n, float C,
                            float* log_ratio, float* k3, float* w, hipStream_t s);
+// Per-response score / keep and per-token weights of a packed stream (one
+// workgroup per response, fixed-order fp64 sum).
+hipError_t launch_mismatch_seq(const float* a, const float* b, int64_t T, const int64_t* cu_seqlens,
+                               int64_t n_seq, bool k3, float C, double tau_seq, double* score,
+                               uint8_t* keep, float* weight, hipStream_t s);
 
 }  // namespace tim

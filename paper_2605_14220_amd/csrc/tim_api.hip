@@ -116,6 +116,16 @@ tim_status tim_mismatch(const float* logp_a, const float* logp_b, int64_t T, flo
   return hip_status(tim::launch_mismatch(logp_a, logp_b, T, C, log_ratio, k3, is_weight, stream));
 }
 
+tim_status tim_mismatch_seq(const float* logp_a, const float* logp_b, int64_t T, const int64_t* cu_seqlens,
+                            int64_t n_seq, int32_t estimator, float C, double tau_seq, double* score,
+                            uint8_t* keep, float* weight, hipStream_t stream) {
+  const tim_status st = tim::validate_mismatch_seq(logp_a, logp_b, T, cu_seqlens, n_seq, estimator, C, tau_seq);
+  if (st != TIM_OK || n_seq == 0) return st;
+  if (!score && !keep && !weight) return TIM_OK;
+  return hip_status(tim::launch_mismatch_seq(logp_a, logp_b, T, cu_seqlens, n_seq, estimator == TIM_EST_K3, C,
+                                             tau_seq, score, keep, weight, stream));
+}
+
 tim_status tim_logits(const void* hidden, const void* w_vocab, int64_t T, int32_t d, int32_t V,
                       float temperature, int32_t order, float* logits, hipStream_t stream) {
   const tim_status st = tim::validate_logits(hidden, w_vocab, T, d, V, temperature, order, logits);

@@ -62,6 +62,18 @@ inline tim_status validate_mismatch(const float* a, const float* b, int64_t T, f
   return TIM_OK;
 }
 
+inline bool valid_estimator(int32_t e) { return e == TIM_EST_K1 || e == TIM_EST_K3; }
+
+inline tim_status validate_mismatch_seq(const float* a, const float* b, int64_t T, const int64_t* cu,
+                                        int64_t n_seq, int32_t estimator, float C, double tau_seq) {
+  if (T < 0 || n_seq < 0 || n_seq > INT32_MAX) return TIM_ERR_SHAPE;
+  if (n_seq == 0) return TIM_OK;
+  if (!cu) return TIM_ERR_NULL;
+  if (T > 0 && (!a || !b)) return TIM_ERR_NULL;
+  if (!valid_estimator(estimator) || !positive_finite(C) || std::isnan(tau_seq)) return TIM_ERR_VALUE;
+  return TIM_OK;
+}
+
 inline tim_status validate_logits(const void* hidden, const void* w, int64_t T, int32_t d,
                                   int32_t V, float temperature, int32_t order, const float* out) {
   if (T < 0) return TIM_ERR_SHAPE;

@@ -38,7 +38,7 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == ["tim_logits", "tim_logprobs", "tim_logprobs_merge", "tim_logprobs_partials",
-                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_status_string"]
+                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_status_string"]
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -148,6 +148,42 @@ def test_mismatch_noops(lib):
     assert lib.tim_mismatch(None, None, 0, 2.0, None, None, None, None) == Status.OK
     # every output NULL: nothing to compute, nothing launched
     assert lib.tim_mismatch(FAKE, FAKE, 8, 2.0, None, None, None, None) == Status.OK
+
+
+def _seq(lib, **kw):
+    a = kw.get("a", FAKE)
+    b = kw.get("b", FAKE)
+    return lib.tim_mismatch_seq(a, b, kw.get("T", 8), kw.get("cu", FAKE), kw.get("n", 2), kw.get("est", 3),
+                                kw.get("C", 2.0), kw.get("tau", 1e-3), FAKE, FAKE, FAKE, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(n=-1), Status.ERR_SHAPE),
+    (dict(n=2 ** 31), Status.ERR_SHAPE),
+    (dict(cu=None), Status.ERR_NULL),
+    (dict(a=None), Status.ERR_NULL),
+    (dict(b=None), Status.ERR_NULL),
+    (dict(est=2), Status.ERR_VALUE),
+    (dict(est=0), Status.ERR_VALUE),
+    (dict(C=0.0), Status.ERR_VALUE),
+    (dict(C=-1.0), Status.ERR_VALUE),
+    (dict(C=math.inf), Status.ERR_VALUE),
+    (dict(C=math.nan), Status.ERR_VALUE),
+    (dict(tau=math.nan), Status.ERR_VALUE),
+])
+def test_mismatch_seq_rejects(lib, kw, expect):
+    assert _seq(lib, **kw) == expect
+
+
+def test_mismatch_seq_noops(lib):
+    # no responses: nothing is read, whatever the pointers
+    assert lib.tim_mismatch_seq(None, None, 0, None, 0, 3, 2.0, 1e-3, None, None, None, None) == Status.OK
+    assert lib.tim_mismatch_seq(None, None, 5, None, 0, 0, -1.0, math.nan, None, None, None, None) == Status.OK
+    # all outputs NULL: validated, nothing enqueued
+    assert lib.tim_mismatch_seq(FAKE, FAKE, 8, FAKE, 2, 1, 2.0, math.inf, None, None, None, None) == Status.OK
+    # T == 0 with responses: logp arrays are never read, may be NULL (still rejected on other errors)
+    assert lib.tim_mismatch_seq(None, None, 0, FAKE, 2, 4, 2.0, 1e-3, None, None, None, None) == Status.ERR_VALUE
 
 
 @pytest.mark.parametrize("kw,expect", [

@@ -128,6 +128,23 @@ def test_stress_invariance_and_mismatch_report():
     r_lr, r_k3, r_w = oracle.mismatch(ref[0].cpu().numpy(), eng[0].cpu().numpy(), 2.0)
     assert np.all(np.abs(lr.double().cpu().numpy() - r_lr) <= 2.0 ** -24 * np.abs(r_lr) + 1e-45)
     assert np.all(np.abs(w.double().cpu().numpy() - r_w) <= TOL_W_REL * r_w)
+    # sequence level over the packed responses (Section 4.2): K1/K3 scores, the
+    # rejection mask at tau_seq = 0.001 and the truncated-and-rejected weights
+    lens = cfg.lengths()
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    a_np, b_np = ref[0].cpu().numpy(), eng[0].cpu().numpy()
+    for est, name in ((tim.Estimator.K1, "k1"), (tim.Estimator.K3, "k3")):
+        sc, kp, wt = tim.mismatch_seq(ref[0], eng[0], torch.as_tensor(cu, device="cuda"), C=2.0, tau_seq=1e-3,
+                                      estimator=est)
+        r_sc, r_kp, r_wt = oracle.mismatch_seq(a_np, b_np, cu, name, 2.0, 1e-3)
+        sc = sc.cpu().numpy()
+        mag = np.abs(r_sc) + 1e-30
+        assert np.all(np.abs(sc - r_sc) <= 1e-9 * np.maximum(mag, np.abs(sc)) + 1e-15), np.max(np.abs(sc - r_sc))
+        clear = np.abs(r_sc - 1e-3) > 1e-12
+        assert (kp.cpu().numpy().astype(bool)[clear] == r_kp[clear]).all()
+        assert np.all(np.abs(wt.double().cpu().numpy() - r_wt) <= TOL_W_REL * r_wt)
+        print(f"[stress] sequence {name}: {len(lens)} responses, score min/median/max = {sc.min():.3e}/"
+              f"{np.median(sc):.3e}/{sc.max():.3e}; rejected at tau_seq=1e-3: {int((~r_kp).sum())}")
 
 
 def test_long_training_vs_decode_batches():
