@@ -11,7 +11,10 @@ Parity status (each function's own docstring names its pins):
 * ``logprobs``      pinned (closed forms, brute force, library routines).
 * ``mismatch``      pinned (Table 1 of the paper, closed forms, series).
 * ``mismatch_seq``  pinned (closed forms, telescoping, brute force, boundaries).
+* ``logit_grads``, ``logprob_grads``  pinned (finite differences of the pinned
+  forward, float64 autograd, closed forms, the zero-sum identity).
 """
 
 from .logprobs import bf16_to_f64, logits, logprobs  # noqa: F401
+from .grads import logit_grads, logprob_grads  # noqa: F401
 from .mismatch import mismatch, mismatch_seq  # noqa: F401

@@ -399,3 +399,143 @@ def test_seq_response_order_is_irrelevant():
     cu2 = np.concatenate([[0], np.cumsum([len(p[0]) for p in pieces])])
     score2, keep2, _ = oracle.mismatch_seq(a2, b2, cu2, "k3", 2.0, 1e-3)
     assert (score2 == score[perm]).all() and (keep2 == keep[perm]).all()
+
+
+# ---------------------------------------------------------------- gradients
+
+def _loss(hb, wb, tok, tau, g, e):
+    lp, H = oracle.logprobs(hb, wb, tok, tau)
+    lp = np.where(np.isnan(lp), 0.0, lp)
+    return float((g * lp).sum() + (e * H).sum())
+
+
+def _grid_bits(shape, seed):
+    """bf16 values k / 256 with 64 <= |k| <= 248: every value +-1/256 and +-2/256
+    is again exact in bf16, so finite differences perturb exactly."""
+    rng = np.random.default_rng(seed)
+    k = rng.integers(64, 249, size=shape) * rng.choice([-1, 1], size=shape)
+    return _bits(k / 256.0)
+
+
+def _fd(f, x_bits, idx, step=1.0 / 256):
+    """Richardson-extrapolated central difference of f at x_bits[idx] (O(step^4))."""
+    x = oracle.bf16_to_f64(x_bits)
+
+    def at(delta):
+        y = x.copy()
+        y[idx] += delta
+        yb = _bits(y)
+        assert oracle.bf16_to_f64(yb)[idx] == y[idx]  # the perturbed value is exact
+        return f(yb)
+    d1 = at(step) - at(-step)
+    d2 = at(2 * step) - at(-2 * step)
+    return (8 * d1 - d2) / (12 * step)
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.7])
+def test_grads_match_finite_differences(tau):
+    """Derivative by definition: perturb every input of a tiny case in the pinned forward."""
+    T, d, V = 3, 8, 6
+    hb, wb = _grid_bits((T, d), 40), _grid_bits((V, d), 41)
+    tok = np.array([0, 3, 5])
+    rng = np.random.default_rng(42)
+    g, e = rng.standard_normal(T), rng.standard_normal(T)
+    dh, dw = oracle.logprob_grads(hb, wb, tok, tau, g, e)
+    for i in range(T):
+        for k in range(d):
+            fd = _fd(lambda xb: _loss(xb, wb, tok, tau, g, e), hb, (i, k))
+            assert abs(fd - dh[i, k]) <= 1e-6 * (1 + abs(fd)), (i, k, fd, dh[i, k])
+    for v in range(V):
+        for k in range(d):
+            fd = _fd(lambda xb: _loss(hb, xb, tok, tau, g, e), wb, (v, k))
+            assert abs(fd - dw[v, k]) <= 1e-6 * (1 + abs(fd)), (v, k, fd, dw[v, k])
+
+
+@pytest.mark.parametrize("tau", [1.0, 0.6])
+def test_grads_match_torch_autograd(tau):
+    """torch autograd in float64 through the textbook forward (log_softmax,
+    gather, entropy) -- a library differentiation, independent of the oracle's
+    closed-form Jacobian."""
+    T, d, V = 7, 48, 37
+    hb, wb = _tiny(T, V, d=d, scale=2.0)
+    tok = np.array([0, 36, 5, -1, 12, 37, 20])  # two out-of-range ids: no logp term
+    rng = np.random.default_rng(5)
+    g, e = rng.standard_normal(T), rng.standard_normal(T)
+    h = torch.tensor(oracle.bf16_to_f64(hb), requires_grad=True)
+    w = torch.tensor(oracle.bf16_to_f64(wb), requires_grad=True)
+    logq = torch.log_softmax((h @ w.T) / tau, dim=1)
+    H = -(logq.exp() * logq).sum(dim=1)
+    ok = torch.tensor((tok >= 0) & (tok < V))
+    lp = logq[torch.arange(T), torch.tensor(np.clip(tok, 0, V - 1))]
+    L = (torch.tensor(g) * torch.where(ok, lp, torch.zeros_like(lp))).sum() + (torch.tensor(e) * H).sum()
+    L.backward()
+    dh, dw = oracle.logprob_grads(hb, wb, tok, tau, g, e)
+    np.testing.assert_allclose(dh, h.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dw, w.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_grads_sum_to_zero_over_vocab():
+    """sum_v dz_v = 0 (softmax gradients): dW's columns sum to zero, and dh does
+    not change when every w_v is shifted by the same vector."""
+    T, d, V = 5, 32, 40
+    hb, wb = _tiny(T, V, d=d)
+    tok = np.array([1, 2, 39, 0, 17])
+    rng = np.random.default_rng(6)
+    g, e = rng.standard_normal(T), rng.standard_normal(T)
+    dacc = oracle.logit_grads(hb, wb, tok, 1.0, g, e)
+    np.testing.assert_allclose(dacc.sum(axis=1), 0.0, atol=1e-14)
+    dh, dw = oracle.logprob_grads(hb, wb, tok, 1.0, g, e)
+    np.testing.assert_allclose(dw.sum(axis=0), 0.0, atol=1e-12)
+    # a common shift of every w_v by a vector c (exact on the k / 256 grid)
+    wg = _grid_bits((V, d), 8)
+    c = np.random.default_rng(9).integers(-4, 5, size=d) / 256.0
+    w2 = oracle.bf16_to_f64(wg) + c
+    wg2 = _bits(w2)
+    np.testing.assert_array_equal(oracle.bf16_to_f64(wg2), w2)
+    dh1, _ = oracle.logprob_grads(hb, wg, tok, 1.0, g, e)
+    dh2, _ = oracle.logprob_grads(hb, wg2, tok, 1.0, g, e)
+    np.testing.assert_allclose(dh2, dh1, atol=1e-12)
+
+
+def test_grads_uniform_row_closed_form():
+    """h = 0: every logit is 0, p = 1/V, H = log V, q + H = 0. Then
+    dh = g (w_a - mean_v w_v) / tau, the entropy gradient vanishes, dW = 0."""
+    T, d, V = 3, 16, 11
+    hb = _bits(np.zeros((T, d)))
+    wb = _rand_bits((V, d), 7)
+    tok = np.array([0, 4, 10])
+    g = np.array([1.0, -2.0, 0.5])
+    e = np.array([3.0, 1.0, -1.0])
+    tau = 0.8
+    dh, dw = oracle.logprob_grads(hb, wb, tok, tau, g, e)
+    w = oracle.bf16_to_f64(wb)
+    exp_dh = g[:, None] * (w[tok] - w.mean(axis=0)) / tau
+    np.testing.assert_allclose(dh, exp_dh, atol=1e-14)
+    np.testing.assert_array_equal(dw, 0.0)
+
+
+@pytest.mark.parametrize("z0,z1", [(0.0, 0.0), (1.5, -0.25), (-3.0, 5.0)])
+def test_grads_two_token_closed_form(z0, z1):
+    """V = 2 is the logistic model: with s = sigmoid(z0 - z1) and token 0,
+    dlogp/dz0 = 1 - s, dlogp/dz1 = s - 1; dH/dz0 = -s (1 - s) (z0 - z1) = -dH/dz1."""
+    hb, wb = _planted([[z0, z1]])
+    s = 1.0 / (1.0 + math.exp(-(z0 - z1)))
+    dacc = oracle.logit_grads(hb, wb, np.array([0]), 1.0, np.array([1.0]), np.array([0.0]))
+    np.testing.assert_allclose(dacc[0], [1 - s, s - 1], atol=1e-15)
+    dacc = oracle.logit_grads(hb, wb, np.array([0]), 1.0, np.array([0.0]), np.array([1.0]))
+    dH0 = -s * (1 - s) * (z0 - z1)
+    np.testing.assert_allclose(dacc[0], [dH0, -dH0], atol=1e-15)
+
+
+def test_grads_linear_in_upstream():
+    T, d, V = 4, 32, 25
+    hb, wb = _tiny(T, V, d=d)
+    tok = np.array([3, 1, 4, 1])
+    rng = np.random.default_rng(9)
+    g1, e1, g2, e2 = (rng.standard_normal(T) for _ in range(4))
+    a = oracle.logit_grads(hb, wb, tok, 1.3, g1, e1)
+    b = oracle.logit_grads(hb, wb, tok, 1.3, g2, e2)
+    c = oracle.logit_grads(hb, wb, tok, 1.3, 2 * g1 - g2, 2 * e1 - e2)
+    np.testing.assert_allclose(c, 2 * a - b, atol=1e-14)
+    z = oracle.logit_grads(hb, wb, tok, 1.3, np.zeros(T), np.zeros(T))
+    np.testing.assert_array_equal(z, 0.0)

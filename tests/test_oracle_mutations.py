@@ -34,6 +34,14 @@ MUTATIONS = [
     ("mismatch.py", "keep[j] = bool(score[j] <= tau_seq)", "keep[j] = bool(score[j] < tau_seq)"),
     ("mismatch.py", "        if keep[j]:\n", "        if True:\n"),
     ("mismatch.py", "else np.expm1(delta) - delta\n", "else np.expm1(delta) + delta\n"),
+    ("grads.py", "* p * (q + H)", "* p * (q - H)"),
+    ("grads.py", "* (onehot - p) - e[r0:r1, None]", "* (onehot - p) + e[r0:r1, None]"),
+    ("grads.py", "gb * (onehot - p)", "gb * onehot"),
+    ("grads.py", "dacc[r0:r1] = dz / float(temperature)", "dacc[r0:r1] = dz * float(temperature)"),
+    ("grads.py", "onehot[rows[ok], tok[ok]] = 1.0", "onehot[rows[ok], np.minimum(tok[ok] + 1, V - 1)] = 1.0"),
+    ("grads.py", "gb = np.where(ok, g[r0:r1], 0.0)", "gb = g[r0:r1]"),
+    ("grads.py", "dw = dacc.T @ h", "dw = dacc.T @ h[::-1]"),
+    ("grads.py", "dh = dacc @ w", "dh = dacc @ w[::-1]"),
 ]
 
 
