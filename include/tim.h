@@ -186,6 +186,66 @@ tim_status tim_mismatch_seq(const float* logp_a, const float* logp_b, int64_t T,
                             float C, double tau_seq,
                             double* score, uint8_t* keep, float* weight, hipStream_t stream);
 
+/* Gradients of the token log-probabilities and entropies (the trainer's side
+ * of Section 2's Eq. 1: the PPO / GRPO objectives of Section 4 differentiate
+ * log pi_train through the ratio, and entropy regularisers the entropy).
+ *
+ * For a scalar loss L with grad_logp[t] = dL/dlogp[t] and grad_entropy[t] =
+ * dL/dentropy[t], and z, p, lse, entropy as in tim_logprobs (same hidden,
+ * w_vocab, tokens, temperature), the gradient with respect to the LM-head
+ * contraction acc = hidden . w_v of row t is
+ *   dlogits[t,v] = ( g ([v == tokens[t]] - p_v) - e p_v (z_v - lse + H) ) / temperature
+ * (g = grad_logp[t], or 0 when tokens[t] is outside [0, V); e = grad_entropy[t];
+ * H = entropy[t]), and
+ *   grad_hidden[t, :] = sum_v dlogits[t,v] w_vocab[v, :]       fp32 [T, d]
+ *   grad_w[v, :]      = sum_t dlogits[t,v] hidden[t, :]        fp32 [V, d]
+ *
+ * lse, entropy  fp32 [T] as returned by tim_logprobs for these inputs (the
+ *          logits are recomputed with the forward's own contraction, so p is
+ *          exactly the forward's); entropy may be NULL when grad_entropy is.
+ * grad_logp fp32 [T] (required); grad_entropy fp32 [T] or NULL (zero).
+ * micro_batch  0 (all T in one pass) or a positive multiple of 128: tokens per
+ *          pass, bounding the workspace; at most 2^22 tokens per pass.
+ * grad_hidden, grad_w  fp32 device outputs, 16-byte aligned; either may be NULL
+ *          (not computed). With accumulate_grad_w = 1 the weight gradient is
+ *          added to grad_w's contents (gradient accumulation), else it
+ *          overwrites them.
+ * workspace  at least tim_logprobs_backward_workspace_size(T, d, V,
+ *          micro_batch) bytes, 16-byte aligned: about
+ *          2 * d * V_pad + 4 * step * V_pad + 2 * d * step bytes with
+ *          V_pad = ceil(V / 256) * 256 and step = min(T, micro_batch).
+ *
+ * Arithmetic: dlogits is formed in fp32 from the recomputed fp32 logits and
+ * rounded once to bf16 (round to nearest even); the two products run on bf16
+ * MFMA with one fp32 accumulation chain per output element, the vocabulary
+ * (for grad_hidden) and the tokens (for grad_w) in ascending order. A row's
+ * grad_hidden is bitwise independent of T, micro_batch and the row's position;
+ * grad_w is bitwise independent of micro_batch (the chain over tokens continues
+ * across passes) and deterministic, with no atomics. Errors: as tim_logprobs;
+ * TIM_ERR_VALUE also for a bad micro_batch or accumulate_grad_w, a misaligned
+ * output, or a pass of more than 2^22 tokens; TIM_ERR_NULL for a missing
+ * lse / grad_logp, or grad_entropy without entropy. T == 0 writes zeros to
+ * grad_w (unless accumulating). */
+size_t tim_logprobs_backward_workspace_size(int64_t T, int32_t d, int32_t V, int64_t micro_batch);
+tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                 int64_t T, int32_t d, int32_t V, float temperature,
+                                 const float* lse, const float* entropy,
+                                 const float* grad_logp, const float* grad_entropy,
+                                 int64_t micro_batch, float* grad_hidden, float* grad_w,
+                                 int32_t accumulate_grad_w, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
+
+/* The first pass of tim_logprobs_backward on its own, for checking it element
+ * by element: writes dlogits (definition above) as bf16 [T, ceil(V / 256) * 256]
+ * row-major (entries past V are 0) into `dlogits` (16-byte aligned). The
+ * workspace holds T * 16 bytes of per-row coefficients. Arguments and errors
+ * as tim_logprobs_backward. */
+tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                           int64_t T, int32_t d, int32_t V, float temperature,
+                           const float* lse, const float* entropy,
+                           const float* grad_logp, const float* grad_entropy,
+                           void* dlogits, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
 /* Test and debugging aid: writes the fp32 logits z[T, V] (row-major) exactly as
  * tim_logprobs forms them before the softmax (same kernel code, same
  * accumulation order, same temperature multiply), for checking the gather and

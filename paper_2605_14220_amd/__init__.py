@@ -83,6 +83,16 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tim_mismatch_seq.restype = c.c_int
     lib.tim_mismatch_seq.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_void_p, c.c_int64, c.c_int32,
                                      c.c_float, c.c_double, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p]
+    lib.tim_logprobs_backward_workspace_size.restype = c.c_size_t
+    lib.tim_logprobs_backward_workspace_size.argtypes = [c.c_int64, c.c_int32, c.c_int32, c.c_int64]
+    lib.tim_logprobs_backward.restype = c.c_int
+    lib.tim_logprobs_backward.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
+                                          c.c_float, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64,
+                                          c.c_void_p, c.c_void_p, c.c_int32, c.c_void_p, c.c_size_t, c.c_void_p]
+    lib.tim_logit_grads.restype = c.c_int
+    lib.tim_logit_grads.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
+                                    c.c_float, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p,
+                                    c.c_void_p, c.c_size_t, c.c_void_p]
     lib.tim_logits.restype = c.c_int
     lib.tim_logits.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32, c.c_float,
                                c.c_int32, c.c_void_p, c.c_void_p]
@@ -240,3 +250,80 @@ def logits(hidden: torch.Tensor, w_vocab: torch.Tensor, temperature: float = 1.0
     _check(lib.tim_logits(_ptr(hidden), _ptr(w_vocab), T, d, V, float(temperature), int(order), _ptr(z),
                           _stream(hidden.device)))
     return z
+
+
+def backward_workspace_size(T: int, d: int, V: int, micro_batch: int = 0) -> int:
+    """Bytes of workspace tim_logprobs_backward needs (0 for T == 0 or invalid arguments)."""
+    return int(load_library().tim_logprobs_backward_workspace_size(int(T), int(d), int(V), int(micro_batch)))
+
+
+def _grad_inputs(name, hidden, w_vocab, tokens, lse, grad_logp, entropy, grad_entropy):
+    if hidden.dtype != torch.bfloat16 or w_vocab.dtype != torch.bfloat16:
+        raise TypeError(f"tim.{name}: hidden and w_vocab must be bfloat16")
+    if tokens.dtype != torch.int32:
+        raise TypeError(f"tim.{name}: tokens must be int32")
+    if hidden.dim() != 2 or w_vocab.dim() != 2 or hidden.shape[1] != w_vocab.shape[1]:
+        raise ValueError(f"tim.{name}: hidden [T, d] and w_vocab [V, d] must share d")
+    T = hidden.shape[0]
+    for t in (tokens, lse, grad_logp, entropy, grad_entropy):
+        if t is not None and t.shape != (T,):
+            raise ValueError(f"tim.{name}: per-row arrays must be [T]")
+    for t in (lse, grad_logp, entropy, grad_entropy):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError(f"tim.{name}: lse, entropy and the upstream gradients must be fp32")
+    _require_gpu(hidden, w_vocab, tokens, lse, grad_logp, entropy, grad_entropy)
+
+
+def logprobs_backward(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor, lse: torch.Tensor,
+                      grad_logp: torch.Tensor, temperature: float = 1.0, entropy: torch.Tensor | None = None,
+                      grad_entropy: torch.Tensor | None = None, micro_batch: int = 0, want_hidden: bool = True,
+                      want_w: bool = True, grad_w: torch.Tensor | None = None, accumulate: bool = False,
+                      workspace: torch.Tensor | None = None):
+    """Gradients of sum_t grad_logp[t] logp[t] + grad_entropy[t] entropy[t] with respect
+    to hidden [T, d] and w_vocab [V, d], as fp32 (grad_hidden or None, grad_w or None).
+
+    lse (and entropy, when grad_entropy is given) are tim.logprobs' outputs for the same
+    inputs. grad_w, if given, is the fp32 [V, d] output buffer; with accumulate=True the
+    gradient is added to its contents. See include/tim.h."""
+    lib = load_library()
+    _grad_inputs("logprobs_backward", hidden, w_vocab, tokens, lse, grad_logp, entropy, grad_entropy)
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    dev = hidden.device
+    gh = torch.empty((T, d), dtype=torch.float32, device=dev) if want_hidden else None
+    if want_w and grad_w is None:
+        if accumulate:
+            raise ValueError("tim.logprobs_backward: accumulate needs the grad_w buffer")
+        grad_w = torch.empty((V, d), dtype=torch.float32, device=dev)
+    gw = grad_w if want_w else None
+    if gw is not None and (gw.dtype != torch.float32 or gw.shape != (V, d)):
+        raise ValueError("tim.logprobs_backward: grad_w must be fp32 [V, d]")
+    _require_gpu(gh, gw, workspace)
+    need = backward_workspace_size(T, d, V, micro_batch)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=dev)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check(lib.tim_logprobs_backward(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature),
+                                     _ptr(lse), _ptr(entropy), _ptr(grad_logp), _ptr(grad_entropy),
+                                     int(micro_batch), _ptr(gh), _ptr(gw), 1 if accumulate else 0,
+                                     _ptr(workspace), ws_bytes, _stream(dev)))
+    return gh, gw
+
+
+def logit_grads(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor, lse: torch.Tensor,
+                grad_logp: torch.Tensor, temperature: float = 1.0, entropy: torch.Tensor | None = None,
+                grad_entropy: torch.Tensor | None = None) -> torch.Tensor:
+    """bf16 [T, ceil(V / 256) * 256] gradients with respect to the LM-head contraction,
+    exactly as the backward's first pass forms them (test/debug aid)."""
+    lib = load_library()
+    _grad_inputs("logit_grads", hidden, w_vocab, tokens, lse, grad_logp, entropy, grad_entropy)
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    dev = hidden.device
+    v_pad = (V + VOCAB_TILE - 1) // VOCAB_TILE * VOCAB_TILE
+    out = torch.empty((T, v_pad), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(max(T * 16, 16), dtype=torch.uint8, device=dev)
+    _check(lib.tim_logit_grads(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature), _ptr(lse),
+                               _ptr(entropy), _ptr(grad_logp), _ptr(grad_entropy), _ptr(out), _ptr(ws),
+                               ws.numel(), _stream(dev)))
+    return out

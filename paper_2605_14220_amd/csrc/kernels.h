@@ -29,6 +29,38 @@ struct LmHeadArgs {
   float* logits;          // [rows, V] for the logits dump, else null
 };
 
+// Backward of the fused log-prob, logit-gradient pass: the LM-head
+// contraction recomputed exactly as the forward forms it, then per entry
+// dacc = gamma [v == token] - p (alpha + beta q), q = z - lse, p = e^q, from
+// the row's words coef = (lse, alpha, beta, gamma); written as bf16.
+struct DlogitsArgs {
+  const void* hidden;     // bf16 [rows, d]
+  const void* w;          // bf16 [V, d]
+  const int32_t* tokens;  // [rows]
+  const void* coef;       // float4 [rows]
+  int64_t rows;
+  int32_t d;
+  int32_t V;
+  float inv_tau;
+  void* dacc;             // bf16 [rows, ld]; entries V .. ld - 1 of a row are written as 0
+  int64_t ld;             // a multiple of 256 covering V
+};
+
+// Plain tile pass: out[j * ldo + i] = (accumulate ? out[j * ldo + i] : 0)
+// + sum_k A[i][k] B[j][k] in one fp32 accumulation chain per element, K
+// ascending; A bf16 [a_rows, K], B bf16 [b_rows, K] row-major, K a multiple
+// of 128, a_rows a multiple of 4.
+struct GemmArgs {
+  const void* a;
+  const void* b;
+  int64_t b_rows;
+  int32_t a_rows;
+  int32_t K;
+  float* out;
+  int64_t ldo;
+  int32_t accumulate;
+};
+
 int n_vocab_tiles(int V);
 
 // Partials of every (row, vocab tile). rows_per_wg in {64, 128, 256} is the
@@ -37,6 +69,20 @@ hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, h
 // Fixed-order merge of each row's partials into logp / entropy / lse.
 hipError_t launch_merge(const Partial* part, const int32_t* tokens, int64_t rows, int V,
                         bool left_fold, float* logp, float* entropy, float* lse, hipStream_t s);
+hipError_t launch_dlogits(const DlogitsArgs& a, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
+// dst[c * ld_dst + r] = src[r * ld_src + c] for r < R, 0 for R <= r < R_pad,
+// c < C (bf16; C and R_pad multiples of 64, 16-byte aligned rows).
+hipError_t launch_transpose(const void* src, int64_t R, int64_t C, int64_t ld_src, void* dst, int64_t R_pad,
+                            int64_t ld_dst, hipStream_t s);
+// Per-row words (lse, alpha, beta, gamma) of the logit gradient for upstream
+// gradients g (of logp) and e (of the entropy; may be null): with g' = g for
+// a token in [0, V) else 0, alpha = (g' + e H) / tau, beta = e / tau,
+// gamma = g' / tau, each formed in fp64 and rounded once.
+hipError_t launch_grad_coef(const float* lse, const float* entropy, const float* grad_logp,
+                            const float* grad_entropy, const int32_t* tokens, int64_t rows, int V,
+                            float temperature, void* coef, hipStream_t s);
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
 hipError_t launch_mismatch(const float* a, const float* b, int64_t n, float C,
                            float* log_ratio, float* k3, float* w, hipStream_t s);
 // Per-response score / keep and per-token weights of a packed stream (one

@@ -1,0 +1,264 @@
+// Backward of the fused LM-head log-probability and entropy for gfx950.
+//
+// For a scalar loss L with upstream gradients g_t = dL/dlogp_t and
+// e_t = dL/dH_t, and the forward's z = acc / tau, q_v = z_v - lse,
+// p_v = e^{q_v}, the chain rule through the softmax gives per row
+//   dacc_v = ( g_t ([v = a_t] - p_v) - e_t p_v (q_v + H_t) ) / tau
+//          = gamma [v = a_t] - p_v (alpha + beta q_v)
+// with gamma = g_t / tau, alpha = (g_t + e_t H_t) / tau, beta = e_t / tau, and
+//   dh_t = sum_v dacc_{t,v} w_v,      dW_v = sum_t dacc_{t,v} h_t.
+// These are the gradients the trainer takes of the same per-token log-probs
+// whose forward values the rollout must match (Section 2, Eq. 1; the PPO and
+// GRPO objectives of Section 4 differentiate log pi_train through the ratio).
+//
+// Three contractions, all on the tile pass (one fp32 chain per element, K
+// ascending, no atomics):
+//   1. lmhead_dlogits: z recomputed with the forward's own main loop (K = d),
+//      so p is formed from exactly the logits whose lse the forward returned;
+//      the epilogue writes dacc as bf16 [rows, V_pad] (the rounding a bf16
+//      trainer applies to logit gradients before the weight products).
+//   2. dh = dacc . W: A = W^T [d, V_pad], B = dacc, K = V_pad. A row's chain
+//      runs over the whole padded vocabulary in one order whatever the batch,
+//      so dh is batch-invariant like the forward.
+//   3. dW = dacc^T . h: A = h^T [d, T_pad], B = dacc^T [V_pad, T_pad],
+//      K = T_pad. The chain over tokens starts from the value already in dW
+//      after the first micro-batch (or with accumulation), so micro-batches of
+//      multiples of 128 tokens continue one chain: dW is bitwise the same for
+//      every such micro-batch size.
+// The transposed operands are written by an LDS-tiled transpose; the padding
+// rows and columns are zeros, which add exactly nothing.
+
+#include "tilepass.h"
+
+namespace tim {
+namespace {
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const __bf16 a = (__bf16)lo, b = (__bf16)hi;  // round to nearest even
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
+// Logit gradients. A = W [V, d], B = hidden states, K = d: the forward's pass.
+// For row block bj a lane holds row (l % 16) and, in register r of W block bi,
+// the vocabulary entry v0 + wv * 128 + bi * 16 + 4 (l / 16) + r; the four
+// registers go out as one 8-byte store.
+struct EpiDlogits {
+  using Args = DlogitsArgs;
+  static constexpr bool kTokens = true;
+  static constexpr bool kCoef = true;
+  template <int BT>
+  static constexpr int scratch_bytes() { return 0; }
+  __device__ static TileOps ops(const Args& a) {
+    return TileOps{a.w, a.hidden, a.tokens, a.coef, a.rows, a.V, a.d};
+  }
+  template <int NTB, int WT>
+  __device__ static void init(const Args&, int64_t, int64_t, f32x4 (&acc)[8][2 * NTB], int, int) {
+#pragma unroll
+    for (int bi = 0; bi < 8; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2 * NTB; ++bj) acc[bi][bj] = f32x4{};
+  }
+  template <int NTB, int WT>
+  __device__ static void epilogue(const Args& a, int, int, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], float*,
+                                  const int* tok_lds, const f32x4* coef_lds, int wave, int lane) {
+    constexpr int NJ = 2 * NTB;
+    const int wv = wave & 1, wt = wave >> 1;
+    const int g = lane >> 4, c16 = lane & 15;
+    const float inv_tau = a.inv_tau;
+    const int64_t vlane = v0 + wv * 128 + 4 * g;
+    const bool full = v0 + kVocabTile <= a.V;
+    uint16_t* out = (uint16_t*)a.dacc;
+#pragma unroll
+    for (int bj = 0; bj < NJ; ++bj) {
+      const int t_loc = wt * NTB * 32 + bj * 16 + c16;
+      const int64_t tg = t0 + t_loc;
+      if (tg >= a.rows) continue;
+      const f32x4 c = coef_lds[t_loc];
+      const float lse = c[0], alpha = c[1], beta = c[2], gamma = c[3];
+      const int64_t tl = (int64_t)tok_lds[t_loc] - vlane;  // the token's offset from this lane's first entry
+      uint16_t* row = out + tg * a.ld + vlane;
+#pragma unroll
+      for (int bi = 0; bi < 8; ++bi) {
+        float o[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float z = acc[bi][bj][r];
+          if (inv_tau != 1.0f) z = z * inv_tau;
+          const float q = z - lse;
+          const float p = exp2_hw(q * kLog2e);
+          const float pw = p * __builtin_fmaf(beta, q, alpha);
+          float dv = (tl == bi * 16 + r) ? gamma - pw : -pw;
+          if (!full && vlane + bi * 16 + r >= a.V) dv = 0.f;
+          o[r] = dv;
+        }
+        *(uint2*)(row + bi * 16) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+      }
+    }
+  }
+};
+
+// fp32 stores of the tile (optionally continuing from the stored values):
+// lane l holds B row j = t0 + wt * NTB * 32 + bj * 16 + l % 16 and the 4
+// consecutive A rows i = v0 + wv * 128 + bi * 16 + 4 (l / 16) + r, one 16-byte
+// access each.
+struct EpiStore {
+  using Args = GemmArgs;
+  static constexpr bool kTokens = false;
+  static constexpr bool kCoef = false;
+  template <int BT>
+  static constexpr int scratch_bytes() { return 0; }
+  __device__ static TileOps ops(const Args& a) {
+    return TileOps{a.a, a.b, nullptr, nullptr, a.b_rows, a.a_rows, a.K};
+  }
+  template <int NTB, int WT>
+  __device__ static void init(const Args& a, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], int wave, int lane) {
+    const int wv = wave & 1, wt = wave >> 1;
+    const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
+#pragma unroll
+    for (int bj = 0; bj < 2 * NTB; ++bj) {
+      const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
+#pragma unroll
+      for (int bi = 0; bi < 8; ++bi) {
+        const int64_t i0 = i_lane + bi * 16;
+        acc[bi][bj] = (a.accumulate && jr < a.b_rows && i0 < a.a_rows) ? *(const f32x4*)(a.out + jr * a.ldo + i0)
+                                                                      : f32x4{};
+      }
+    }
+  }
+  template <int NTB, int WT>
+  __device__ static void epilogue(const Args& a, int, int, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], float*,
+                                  const int*, const f32x4*, int wave, int lane) {
+    const int wv = wave & 1, wt = wave >> 1;
+    const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
+#pragma unroll
+    for (int bj = 0; bj < 2 * NTB; ++bj) {
+      const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
+      if (jr >= a.b_rows) continue;
+#pragma unroll
+      for (int bi = 0; bi < 8; ++bi) {
+        const int64_t i0 = i_lane + bi * 16;
+        if (i0 < a.a_rows) *(f32x4*)(a.out + jr * a.ldo + i0) = acc[bi][bj];
+      }
+    }
+  }
+};
+
+template <int NTB, int WT>
+__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, false>::PER_CU))
+void lmhead_dlogits(DlogitsArgs a, int n_vt, int n_tt) {
+  tile_pass<NTB, WT, false, EpiDlogits>(a, n_vt, n_tt);
+}
+
+template <int NTB, int WT>
+__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, false>::PER_CU))
+void gemm_nt_f32(GemmArgs a, int n_vt, int n_tt) {
+  tile_pass<NTB, WT, false, EpiStore>(a, n_vt, n_tt);
+}
+
+// 64 x 64 bf16 tile per workgroup: 16-byte row loads into LDS, then each
+// thread gathers 8 consecutive source rows of one column into one 16-byte
+// store of the destination row.
+__global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict__ src, int64_t R, int64_t ld_src,
+                                                      uint16_t* __restrict__ dst, int64_t ld_dst) {
+  __shared__ uint16_t t[64][66];
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int idx = tid + 256 * s;
+    const int rr = idx >> 3, cc = (idx & 7) * 8;
+    uint4 v = uint4{0u, 0u, 0u, 0u};
+    if (r0 + rr < R) v = *(const uint4*)(src + (r0 + rr) * ld_src + c0 + cc);
+    uint32_t* d = (uint32_t*)&t[rr][cc];
+    d[0] = v.x;
+    d[1] = v.y;
+    d[2] = v.z;
+    d[3] = v.w;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int idx = tid + 256 * s;
+    const int cc = idx >> 3, rr = (idx & 7) * 8;
+    uint32_t w[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) w[k] = (uint32_t)t[rr + 2 * k][cc] | ((uint32_t)t[rr + 2 * k + 1][cc] << 16);
+    *(uint4*)(dst + (c0 + cc) * ld_dst + r0 + rr) = uint4{w[0], w[1], w[2], w[3]};
+  }
+}
+
+__global__ __launch_bounds__(256) void grad_coef_kernel(const float* __restrict__ lse, const float* __restrict__ ent,
+                                                        const float* __restrict__ g, const float* __restrict__ e,
+                                                        const int32_t* __restrict__ tok, int64_t rows, int V,
+                                                        double tau, f32x4* __restrict__ coef) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= rows) return;
+  const int a = tok[t];
+  const double gl = (a >= 0 && a < V) ? (double)g[t] : 0.0;
+  const double ev = e ? (double)e[t] : 0.0;
+  const double eh = e ? ev * (double)ent[t] : 0.0;
+  coef[t] = f32x4{lse[t], (float)((gl + eh) / tau), (float)(ev / tau), (float)(gl / tau)};
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) p[i] = 0.f;
+}
+
+}  // namespace
+
+template <class E, int NTB, int WT>
+static hipError_t launch_pass(void (*kernel)(typename E::Args, int, int), const typename E::Args& a, int64_t a_rows,
+                              int64_t b_rows, hipStream_t s) {
+  constexpr int BT = Tile<NTB, WT>::BT;
+  const int64_t n_vt = (a_rows + kVocabTile - 1) / kVocabTile;
+  const int64_t n_tt = (b_rows + BT - 1) / BT;
+  const int64_t nblk = n_vt * n_tt;
+  if (nblk > 0x7fffffff) return hipErrorInvalidValue;
+  int64_t grid = nblk;
+  const int64_t resident = (int64_t)device_cu_count() * Shape<NTB, WT, false>::PER_CU;
+  if (resident > 0 && resident < grid) grid = resident;
+  hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(128 * WT), 0, s, a, (int)n_vt, (int)n_tt);
+  return hipGetLastError();
+}
+
+hipError_t launch_dlogits(const DlogitsArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  return launch_pass<EpiDlogits, 2, 4>(lmhead_dlogits<2, 4>, a, a.V, a.rows, s);
+}
+
+hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.b_rows <= 0 || a.a_rows <= 0) return hipSuccess;
+  return launch_pass<EpiStore, 2, 4>(gemm_nt_f32<2, 4>, a, a.a_rows, a.b_rows, s);
+}
+
+hipError_t launch_transpose(const void* src, int64_t R, int64_t C, int64_t ld_src, void* dst, int64_t R_pad,
+                            int64_t ld_dst, hipStream_t s) {
+  if (C % 64 != 0 || R_pad % 64 != 0 || R > R_pad) return hipErrorInvalidValue;
+  if (C == 0 || R_pad == 0) return hipSuccess;
+  if (R_pad / 64 > 0x7fffffff || C / 64 > 65535) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(transpose_bf16, dim3((unsigned)(R_pad / 64), (unsigned)(C / 64)), dim3(256), 0, s,
+                     (const uint16_t*)src, R, ld_src, (uint16_t*)dst, ld_dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_grad_coef(const float* lse, const float* entropy, const float* grad_logp,
+                            const float* grad_entropy, const int32_t* tokens, int64_t rows, int V,
+                            float temperature, void* coef, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int64_t nb = (rows + 255) / 256;
+  if (nb > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(grad_coef_kernel, dim3((unsigned)nb), dim3(256), 0, s, lse, entropy, grad_logp, grad_entropy,
+                     tokens, rows, V, (double)temperature, (f32x4*)coef);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t nb = (n + 255) / 256;
+  if (nb > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)nb), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+}  // namespace tim

@@ -32,308 +32,11 @@
 // order, then over the lane groups (lane ^ 16, then lane ^ 32); the two waves'
 // partials are then merged, lower vocabulary half first.
 
-#include "kernels.h"
+
+#include "tilepass.h"
 
 namespace tim {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-// Buffer resources exist only in the device pass; the host pass compiles the
-// kernels as launch stubs and never runs their bodies.
-#if defined(__HIP_DEVICE_COMPILE__)
-typedef __amdgpu_buffer_rsrc_t rsrc_t;
-#else
-struct rsrc_t {
-  int w[4];
-};
-#endif
-
-// Compile-time launch and pipeline shape. None of these changes the
-// arithmetic: the hidden dimension is accumulated in the same ascending
-// 32-element MFMA steps whatever the buffer count, LDS swizzle or tile order.
-#ifndef TIM_NBUF
-#define TIM_NBUF 2         // LDS stage buffers: a power of two >= 2 (as many as fit, up to this)
-#endif
-#ifndef TIM_GROUP_V
-#define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
-#endif
-#ifndef TIM_LOAD_AUX
-#define TIM_LOAD_AUX 0     // cache-policy bits of the global->LDS loads (gfx950 sc0=1, nt=2, sc1=16)
-#endif
-#ifndef TIM_PERSISTENT
-#define TIM_PERSISTENT 1   // full-size launches: one workgroup per CU looping over tiles
-#endif
-#ifndef TIM_WIDE_WAVES
-#define TIM_WIDE_WAVES 1   // 256-row tiles: 8 waves of 128x64 (2 per SIMD); 0 = 4 waves of 128x128
-#endif
-
-constexpr int kKS = 64;                  // hidden-dimension elements per LDS stage
-constexpr int kRowBytes = kKS * 2;       // bytes of one row in one stage
-constexpr int kChunks = kRowBytes / 16;  // 16-byte chunks per row per stage
-constexpr int kKM = 32;                  // hidden-dimension elements per MFMA
-constexpr int kSteps = kKS / kKM;        // MFMA k-steps per stage
-constexpr int kWBytes = kVocabTile * kRowBytes;
-static_assert(kSteps == 2, "the operand double buffer alternates once per k-step");
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kNegInf = -__builtin_inff();
-
-// Workgroup shape: 2 waves along the vocab tile (128 entries, 8 blocks of 16,
-// each) times WT waves along the rows, each wave holding NTB * 32 rows (2 * NTB
-// blocks of 16).
-template <int NTB, int WT>
-struct Tile {
-  static constexpr int NW = 2 * WT;            // waves per workgroup
-  static constexpr int NJ = 2 * NTB;           // row blocks of 16 per wave
-  static constexpr int BT = WT * NTB * 32;     // rows per workgroup
-  static constexpr int kHBytes = BT * kRowBytes;
-  static constexpr int kStageBytes = kWBytes + kHBytes;
-};
-
-// Residency and pipeline depth of one kernel shape. Shapes whose wave holds
-// at most 128 x 64 accumulators (and no second accumulator set) run two
-// workgroups per CU when two stage buffers fit in half of the 160 KB LDS.
-template <int NTB, int WT, bool SPLITK4>
-struct Shape {
-  using TL = Tile<NTB, WT>;
-  static constexpr int PER_CU =
-      (WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1;
-  static constexpr int FIT = (160 * 1024 / PER_CU) / TL::kStageBytes;
-  static constexpr int CAP = FIT < TIM_NBUF ? FIT : TIM_NBUF;
-  // a power of two, so that it divides the stage count
-  static constexpr int NBUF = CAP >= 8 ? 8 : CAP >= 4 ? 4 : 2;
-  static_assert(FIT >= 2, "double buffering at least");
-};
-
-// 16-byte chunk c of row r sits at physical chunk c ^ swz(r) of that row. A
-// ds_read_b128 serves 16 lanes per cycle; its 16 lanes read 16 consecutive
-// rows at one logical chunk, and with 128-byte rows this swizzle puts them in
-// 16 distinct 16-byte bank groups of the 64 banks.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & (kChunks - 1); }
-
-// s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their maxima): at most N of
-// this wave's vector-memory loads (here: global->LDS DMA) are still in flight.
-template <int N>
-__device__ __forceinline__ void wait_vmem() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
-}
-
-// s_waitcnt vmcnt(N) lgkmcnt(0): additionally every LDS access of this wave done.
-template <int N>
-__device__ __forceinline__ void wait_lgkm0_vmem() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0070);
-}
-
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
-
-// Combine a value over the four lane groups (lanes l, l ^ 16, l ^ 32, l ^ 48)
-// as (g0 op g1) op (g2 op g3). v_permlane16_swap / v_permlane32_swap of a
-// register with itself return, in every lane, the two halves' values in the
-// same order, so every lane computes the same operation on the same operands.
-__device__ __forceinline__ float group_sum(float x) {
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
-}
-__device__ __forceinline__ float group_max(float x) {
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
-  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
-}
-
-// Workgroup barrier between pipeline stages. Each wave has already waited
-// for what the barrier must order (its own DMA of the next stage, and its own
-// reads of the buffer about to be refilled), so no memory fence is needed;
-// the empty asm statements keep the compiler from moving memory operations
-// across it, and the scheduling fences keep every other instruction on its
-// side too.
-__device__ __forceinline__ void stage_barrier() {
-  __builtin_amdgcn_sched_barrier(0);
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_sched_barrier(0);
-  // the k-step after a boundary runs at raised priority (see region_a_prio)
-  __builtin_amdgcn_s_setprio(1);
-}
-
-// Wave priority of the k-step before a boundary. The two waves sharing a SIMD
-// drift apart (the older one issues first); a wave that is already into the
-// next stage's first k-step yields to its sibling still finishing the k-step
-// after the last boundary, so the two reach the next barrier closer together
-// and the time one of them idles there -- with the other issuing MFMAs alone,
-// which does not fill the pipe -- shrinks.
-__device__ __forceinline__ void region_a_prio() { __builtin_amdgcn_s_setprio(0); }
-
-// Tile order: logical id -> (vocab tile, row tile), walking groups of
-// TIM_GROUP_V vocab tiles with the row tiles outer and the vocab tiles inner,
-// so that the workgroups resident on one XCD at a time (consecutive logical
-// ids, see lmhead_partials) share W tiles and hidden-state tiles through that
-// XCD's L2.
-__device__ __forceinline__ void tile_of_lid(int lid, int n_vt, int n_tt, int& vt, int& tt) {
-  constexpr int GV = TIM_GROUP_V;
-  const int group = lid / (GV * n_tt);
-  const int first = group * GV;
-  const int gv = (n_vt - first) < GV ? (n_vt - first) : GV;
-  const int local = lid - group * GV * n_tt;
-  vt = first + local % gv;
-  tt = local / gv;
-}
-
-// Per-lane byte offsets of this wave's DMA loads, relative to the tile's
-// first row at hidden index 0. They do not change along the hidden dimension:
-// each stage only moves the scalar offset.
-template <int NTB, int WT>
-struct LoadPlan {
-  static constexpr int NW = Tile<NTB, WT>::NW;
-  static constexpr int WB = 4 * kChunks / NW;                         // W blocks of 1 KB per wave
-  static constexpr int HB = Tile<NTB, WT>::BT * kChunks / (64 * NW);  // hidden-state blocks per wave
-  static constexpr int L = WB + HB;                                   // DMA loads per wave per stage
-  uint32_t w_off[WB];
-  uint32_t h_off[HB];
-};
-
-template <int NTB, int WT>
-__device__ __forceinline__ LoadPlan<NTB, WT> make_load_plan(int w_rows, int h_rows, int d, int wave, int lane) {
-  LoadPlan<NTB, WT> pl;
-#pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q) {
-    const int p = (wave * LoadPlan<NTB, WT>::WB + q) * 64 + lane;
-    int r = p / kChunks;
-    const int c = (p % kChunks) ^ swz(r);
-    if (r >= w_rows) r = w_rows - 1;  // rows past V: a valid row, masked in the epilogue
-    pl.w_off[q] = (uint32_t)(r * d + c * 8) * 2u;
-  }
-#pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q) {
-    const int p = (wave * LoadPlan<NTB, WT>::HB + q) * 64 + lane;
-    int r = p / kChunks;
-    const int c = (p % kChunks) ^ swz(r);
-    if (r >= h_rows) r = h_rows - 1;  // rows past the batch: never written out
-    pl.h_off[q] = (uint32_t)(r * d + c * 8) * 2u;
-  }
-  return pl;
-}
-
-// Buffer resource over [base, base + bytes): loads outside it return zeros.
-__device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  const uint32_t n = bytes > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)bytes;
-  // dword 3 = 0x00020000: raw (unswizzled) 32-bit-format buffer, the gfx9 encoding.
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)n, 0x00020000);
-#else
-  return rsrc_t{};
-#endif
-}
-
-// Load q of a stage request: the wave's L DMA loads of a stage, W blocks first.
-template <int NTB, int WT>
-__device__ __forceinline__ void request_load(unsigned char* buf, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl,
-                                             int wave, int soff, int q) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int WB = LoadPlan<NTB, WT>::WB;
-  constexpr int L = LoadPlan<NTB, WT>::L;
-  if (q < WB)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff, 0,
-                                             TIM_LOAD_AUX);
-  else
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWBytes + (wave * (L - WB) + (q - WB)) * 1024), 16,
-                                             pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
-#endif
-}
-
-// The tile's BT tokens into LDS, 64 per wave from the first BT / 64 waves
-// (rows past the batch read as 0 and are never used).
-template <int BT>
-__device__ __forceinline__ void request_tokens(int* dst, rsrc_t tr, int wave, int lane) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  if (wave < BT / 64)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(tr, (lds_void*)(dst + wave * 64), 4, (uint32_t)(wave * 64 + lane) * 4u, 0,
-                                             0, 0);
-#endif
-}
-
-// MFMA operands of k-step s of a stage buffer, 8 bf16 per lane: lane l reads
-// row (l % 16) of a 16-row block at hidden offset 32 s + 8 (l / 16).
-__device__ __forceinline__ bf16x8 read_operand(const unsigned char* base, int row, int s, int lane) {
-  const int c = (4 * s + (lane >> 4)) ^ swz(row);
-  return *(const bf16x8*)(base + row * kRowBytes + c * 16);
-}
-// W block bi (16 vocabulary rows) of vocab wave wv
-__device__ __forceinline__ bf16x8 read_a(const unsigned char* buf, int s, int bi, int wv, int lane) {
-  return read_operand(buf, wv * 128 + bi * 16 + (lane & 15), s, lane);
-}
-// hidden-state block bj (16 rows) of row wave wt
-template <int NTB>
-__device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj, int wt, int lane) {
-  return read_operand(buf + kWBytes, wt * NTB * 32 + bj * 16 + (lane & 15), s, lane);
-}
-
-// One k-step as 8 * NJ scheduling units, each pinned on its own: unit i
-// issues the MFMA of W block bi = i / NJ and row block bj = i % NJ (the
-// accumulation order of every logit is the k-step order; the order of the
-// units only interleaves independent chains), then, with LOAD, its share of
-// the DMA loads of a stage request into `lb`, and, with READ, the reads of
-// k-step `rs` of buffer `rb`. Operands alternate between two register sets by
-// k-step parity P: the row-block operands always, read from the first units
-// on; the W operands too with AD (then read right after the row blocks, so
-// every read lands early), else the single W set is refilled block by block
-// right after each block's last use here.
-template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true>
-__device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
-                                      unsigned char* lb, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl, int soff,
-                                      const unsigned char* rb, int rs, int wave, int wv, int wt, int lane) {
-  constexpr int NJ = 2 * NTB;
-  constexpr int NM = 8 * NJ;
-  constexpr int L = LoadPlan<NTB, WT>::L;
-  constexpr int PA = AD ? P : 0, PN = AD ? (P ^ 1) : 0;
-  static_assert(L <= NM, "at most one DMA load per unit");
-#pragma unroll
-  for (int i = 0; i < NM; ++i) {
-    const int bi = i / NJ, bj = i % NJ;
-    acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[PA][bi], fb[P][bj], acc[bi][bj], 0, 0, 0);
-    if (LOAD) {  // load q goes with unit q * NM / L
-      const int q = (i * L + NM - 1) / NM;
-      if (q < L && q * NM / L == i) request_load<NTB, WT>(lb, wr, hr, pl, wave, soff, q);
-    }
-    if (READ) {
-      if (!AD && i < NJ) fb[P ^ 1][i] = read_b<NTB>(rb, rs, i, wt, lane);
-      if (AD) {
-        // NJ + 8 reads spread evenly over the units, in the order the next
-        // k-step consumes them: a0, b0 .. b[NJ-1], a1 .. a7
-        constexpr int NR = NJ + 8;
-        const int r = (i * NR + NM - 1) / NM;
-        if (r < NR && r * NM / NR == i) {
-          if (r == 0) fa[PN][0] = read_a(rb, rs, 0, wv, lane);
-          else if (r <= NJ) fb[P ^ 1][r - 1] = read_b<NTB>(rb, rs, r - 1, wt, lane);
-          else fa[PN][r - NJ] = read_a(rb, rs, r - NJ, wv, lane);
-        }
-      } else {
-        if (bj == NJ - 1) fa[PN][bi] = read_a(rb, rs, bi, wv, lane);
-      }
-    }
-    __builtin_amdgcn_sched_barrier(0);
-  }
-}
-
-// SPLITK4: after each quarter of the hidden dimension, fold the quarter's
-// accumulator into the running sum: ((q0 + q1) + q2) + q3.
-template <int NTB>
-__device__ __forceinline__ void quarter_fold(f32x4 (&acc)[8][2 * NTB], f32x4 (&sum)[8][2 * NTB], int q) {
-#pragma unroll
-  for (int bi = 0; bi < 8; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2 * NTB; ++bj) {
-      if (q == 0) sum[bi][bj] = acc[bi][bj];
-      else sum[bi][bj] = sum[bi][bj] + acc[bi][bj];
-      acc[bi][bj] = f32x4{};
-    }
-}
 
 struct MSU {
   float m, s, u;
@@ -486,205 +189,41 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
   }
 }
 
-template <int NTB, int WT>
-struct TileCtx {
-  int vt;
-  int64_t v0, t0;
-  LoadPlan<NTB, WT> pl;
-  rsrc_t wr, hr, tr;
-};
-
-template <int NTB, int WT>
-__device__ __forceinline__ TileCtx<NTB, WT> make_tile(const LmHeadArgs& a, int lid, int n_vt, int n_tt, int wave,
-                                                      int lane) {
-  constexpr int BT = Tile<NTB, WT>::BT;
-  // Opaque copies: every call recomputes its context instead of the compiler
-  // reusing (and keeping live) the result of an earlier call.
-  asm volatile("" : "+s"(lid));
-  asm volatile("" : "+v"(lane));
-  TileCtx<NTB, WT> c;
-  int tt;
-  tile_of_lid(lid, n_vt, n_tt, c.vt, tt);
-  c.v0 = (int64_t)c.vt * kVocabTile;
-  c.t0 = (int64_t)tt * BT;
-  const int w_rows = (a.V - c.v0) < kVocabTile ? (int)(a.V - c.v0) : kVocabTile;
-  const int h_rows = (a.rows - c.t0) < BT ? (int)(a.rows - c.t0) : BT;
-  c.pl = make_load_plan<NTB, WT>(w_rows, h_rows, a.d, wave, lane);
-  c.wr = make_rsrc((const __bf16*)a.w + c.v0 * a.d, (uint64_t)w_rows * a.d * 2);
-  c.hr = make_rsrc((const __bf16*)a.hidden + c.t0 * a.d, (uint64_t)h_rows * a.d * 2);
-  c.tr = make_rsrc(a.tokens + c.t0, (uint64_t)h_rows * 4);
-  return c;
-}
-
-// Partials of a sequence of (vocab tile, row tile) output tiles. The logical
-// tile ids are dealt to the 8 XCDs in contiguous chunks, and within an XCD
-// round-robin to its workgroups, so at any time the workgroups of one XCD work
-// on consecutive ids. With one workgroup per tile this is a plain launch; with
-// a grid of one workgroup per CU it is persistent, and the stage pipeline then
-// runs on across tiles: the last stages of a tile already request the next
-// tile's first stages, which land while this tile's epilogue runs.
+// Epilogue policies of a tile pass. Each one names the pass's operands, the
+// LDS it needs beside the stage buffers, the per-row data it wants staged in
+// LDS with each tile, how the accumulators start, and what it does with them.
 //
-// Pipeline. Stage s of a tile (kKS hidden-dimension elements of its W and
-// hidden-state rows) lives in LDS buffer s % kNBuf. Each stage has a boundary
-// before its last k-step: every wave waits for its own reads of the stage and
-// for its own DMA of stage s + 1, then the workgroup barrier makes stage s + 1
-// visible and frees buffer s % kNBuf, which takes stage s + kNBuf, its loads
-// spread over that last k-step. MFMA operands are read one k-step ahead,
-// across the boundary too. Requests past the tile go to the next tile's
-// stages, or, with none, re-read the tile's own stages into the freed buffer,
-// so every boundary's wait counts stay the same.
-template <int NTB, int WT, bool SPLITK4, bool DUMP>
-__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
-void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
-  using TL = Tile<NTB, WT>;
-  using LP = LoadPlan<NTB, WT>;
-  using TC = TileCtx<NTB, WT>;
-  constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
-  static_assert((128 / kKS) % kNBuf == 0, "the stage count (a multiple of 128 / kKS) must be a multiple of kNBuf");
-  constexpr int NJ = TL::NJ;
-  constexpr int BT = TL::BT;
-  constexpr int SB = TL::kStageBytes;
-  constexpr int EPI = 7 * BT * 4;
-  constexpr int L = LP::L;
-  // Epilogue scratch of its own when it fits, so the next tile's stages can
-  // land during the epilogue; otherwise it reuses the first stage buffer.
-  constexpr bool kSep = kNBuf * SB + EPI + (DUMP ? 0 : 2 * BT * 4) <= (160 * 1024) / Shape<NTB, WT, SPLITK4>::PER_CU;
-  // With its own scratch, the epilogue also finds the tile's tokens staged
-  // in LDS (two slots, alternating per tile), requested with the tile's first
-  // stage, so it never waits on a global load behind the next tile's stages.
-  constexpr bool kTokLds = kSep && !DUMP;
-  constexpr int TOKB = kTokLds ? 2 * BT * 4 : 0;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[kNBuf * SB + (kSep ? EPI : 0) + TOKB];
-  float* scratch = (float*)(kSep ? lds + kNBuf * SB : lds);
-  int* tok_slot = (int*)(lds + kNBuf * SB + (kSep ? EPI : 0));  // [2][BT] when kTokLds
-  int par = 0;
-
-  const int lane0 = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wv = wave & 1, wt = wave >> 1;
-
-  // this workgroup's tiles: start + wi, start + wi + w_x, ... below start + t_x
-  const int n_tiles = n_vt * n_tt;
-  const int x = blockIdx.x & 7, wi = blockIdx.x >> 3;
-  const int w_x = (int)(gridDim.x >> 3) + (x < (int)(gridDim.x & 7) ? 1 : 0);
-  const int tq = n_tiles >> 3, trm = n_tiles & 7;
-  const int t_x = tq + (x < trm ? 1 : 0);
-  const int start = x * tq + (x < trm ? x : trm);
-  int j = wi;
-  if (j >= t_x) return;
-
-  const int nk = a.d / kKS;  // stages per tile; a multiple of kNBuf
-  const int nk_q = nk / 4;   // stages per quarter (SPLITK4)
-  constexpr int kStep = kKS * 2;
-
-  TC cur = make_tile<NTB, WT>(a, start + j, n_vt, n_tt, wave, lane0);
-
-  // prologue: the tile's tokens and stages 0 .. kNBuf - 1
-  auto prologue = [&]() {
-    if constexpr (kTokLds) request_tokens<BT>(tok_slot + par * BT, cur.tr, wave, lane0);
-#pragma unroll
-    for (int s = 0; s < kNBuf; ++s)
-#pragma unroll
-      for (int q = 0; q < L; ++q)
-        request_load<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q);
-    wait_vmem<(kNBuf - 1) * L>();  // stage 0 landed
-    __syncthreads();
-  };
-  prologue();
-
-  f32x4 acc[8][NJ];
-  f32x4 sum[8][SPLITK4 ? NJ : 1];
-  // One wave per SIMD (four waves) leaves registers for a second W operand set.
-  constexpr bool kAD = TL::NW == 4 && Shape<NTB, WT, SPLITK4>::PER_CU == 1;
-  bf16x8 fa[2][8];   // W operands by k-step parity (with kAD), else fa[0] refilled in place
-  bf16x8 fb[2][NJ];  // hidden-state operands, double buffered by k-step parity
-  while (true) {
-    // Per-tile lane arithmetic is recomputed inside the loop rather than
-    // hoisted out of it (which would keep it live across the whole loop and
-    // push the epilogue into spills): the empty asm hides that the lane index
-    // is loop-invariant.
-    int lane = lane0;
-    asm volatile("" : "+v"(lane));
-    // The next tile's context is rebuilt where it is needed (cheap integer
-    // work) rather than kept live across the loop.
-    const bool has_next = j + w_x < t_x;
-    const int next_lid = start + j + w_x;
+// EpiPartials: the LM head forward. A = W [V, d], B = hidden states, K = d;
+// the epilogue forms the tile's softmax partials (or, DUMP, writes logits).
+template <bool DUMP>
+struct EpiPartials {
+  using Args = LmHeadArgs;
+  static constexpr bool kTokens = !DUMP;
+  static constexpr bool kCoef = false;
+  template <int BT>
+  static constexpr int scratch_bytes() { return 7 * BT * 4; }
+  __device__ static TileOps ops(const Args& a) {
+    return TileOps{a.w, a.hidden, a.tokens, nullptr, a.rows, a.V, a.d};
+  }
+  template <int NTB, int WT>
+  __device__ static void init(const Args&, int64_t, int64_t, f32x4 (&acc)[8][2 * NTB], int, int) {
 #pragma unroll
     for (int bi = 0; bi < 8; ++bi)
 #pragma unroll
-      for (int bj = 0; bj < NJ; ++bj) acc[bi][bj] = f32x4{};
-
-    // stage 0 has landed and is visible: after the prologue, or, when the
-    // pipeline runs on from the previous tile, since its last boundary
-#pragma unroll
-    for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = read_b<NTB>(lds, 0, bj, wt, lane);
-#pragma unroll
-    for (int bi = 0; bi < 8; ++bi) fa[0][bi] = read_a(lds, 0, bi, wv, lane);
-    int k = 0;
-    // steady state: every request is a stage of this tile
-    for (; k + kNBuf < nk; ++k) {
-      unsigned char* cb = lds + (k % kNBuf) * SB;
-      region_a_prio();
-      kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
-      wait_lgkm0_vmem<(kNBuf - 2) * L>();
-      stage_barrier();
-      kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
-                                   lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
-      if constexpr (SPLITK4) {
-        if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
-      }
-    }
-    // tail: the last kNBuf stages, whose requests reach past the tile: to the
-    // next tile's first stages or, with no next tile (or no LDS to keep them
-    // through the epilogue), to this tile's own stages again. Stage k sits in
-    // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
-    {
-      const TC nx = make_tile<NTB, WT>(a, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
-#pragma unroll
-      for (int t = 0; t < kNBuf; ++t) {
-        k = nk - kNBuf + t;
-        unsigned char* cb = lds + t * SB;
-        region_a_prio();
-        kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
-        wait_lgkm0_vmem<(kNBuf - 2) * L>();
-        stage_barrier();
-        // request k + kNBuf: stage t of the next tile (with its tokens)
-        if constexpr (kTokLds) {
-          if (t == 0) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
-        }
-        if (t + 1 < kNBuf)
-          kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
-                                       wave, wv, wt, lane);
-        else
-          kstep<NTB, WT, 1, kAD, true, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
-                                              wt, lane);
-        if constexpr (SPLITK4) {
-          if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
-        }
-      }
-    }
-    if constexpr (SPLITK4) {
-#pragma unroll
-      for (int bi = 0; bi < 8; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < NJ; ++bj) acc[bi][bj] = sum[bi][bj];
-    }
-    if constexpr (!kSep) {
-      wait_vmem<0>();  // every request landed: the epilogue reuses the first buffer
-      __syncthreads();
-    }
-    tile_epilogue<NTB, WT, DUMP>(a, n_vt, cur.vt, cur.v0, cur.t0, acc, scratch,
-                                 kTokLds ? tok_slot + par * BT : nullptr, wave, lane);
-    par ^= 1;
-    if (!has_next) break;
-    j += w_x;
-    cur = make_tile<NTB, WT>(a, next_lid, n_vt, n_tt, wave, lane);
-    if constexpr (!kSep) {
-      __syncthreads();  // the epilogue's reads of the first buffer are done
-      prologue();
-    }
+      for (int bj = 0; bj < 2 * NTB; ++bj) acc[bi][bj] = f32x4{};
   }
-  wait_vmem<0>();  // no global->LDS request may outlive the workgroup
+  template <int NTB, int WT>
+  __device__ static void epilogue(const Args& a, int n_vt, int vt, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB],
+                                  float* scratch, const int* tok_lds, const f32x4*, int wave, int lane) {
+    tile_epilogue<NTB, WT, DUMP>(a, n_vt, vt, v0, t0, acc, scratch, tok_lds, wave, lane);
+  }
+};
+
+// Softmax partials (or, DUMP, logits) of every (vocab tile, row tile).
+template <int NTB, int WT, bool SPLITK4, bool DUMP>
+__global__ __launch_bounds__(128 * WT, (Shape<NTB, WT, SPLITK4>::PER_CU))
+void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
+  tile_pass<NTB, WT, SPLITK4, EpiPartials<DUMP>>(a, n_vt, n_tt);
 }
 
 // ---------------------------------------------------------------- merge
@@ -754,18 +293,6 @@ __global__ __launch_bounds__(256) void lmhead_merge_fold(const Partial* __restri
 }  // namespace
 
 int n_vocab_tiles(int V) { return (V + kVocabTile - 1) / kVocabTile; }
-
-// Compute units of the current device (cached per device).
-static int device_cu_count() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
-  static int cache[64] = {0};
-  if (dev < 64 && cache[dev] > 0) return cache[dev];
-  int n = 0;
-  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (dev < 64) cache[dev] = n;
-  return n;
-}
 
 template <int NTB, int WT, bool SPLITK4, bool DUMP>
 static hipError_t launch_partials_t(const LmHeadArgs& a, bool persistent, hipStream_t s) {

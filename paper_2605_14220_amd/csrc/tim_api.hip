@@ -144,6 +144,119 @@ tim_status tim_logits(const void* hidden, const void* w_vocab, int64_t T, int32_
   return hip_status(tim::launch_partials(a, 128, splitk4, stream));
 }
 
+size_t tim_logprobs_backward_workspace_size(int64_t T, int32_t d, int32_t V, int64_t micro_batch) {
+  if (T <= 0 || tim::check_shape(T, d, V, TIM_ORDER_INVARIANT) != TIM_OK) return 0;
+  if (!tim::valid_backward_micro_batch(micro_batch)) return 0;
+  const tim::BackwardLayout l = tim::backward_layout(T, d, V, micro_batch);
+  return l.step > tim::kMaxBackwardStep ? 0 : l.total;
+}
+
+tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T, int32_t d,
+                           int32_t V, float temperature, const float* lse, const float* entropy,
+                           const float* grad_logp, const float* grad_entropy, void* dlogits, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream) {
+  const tim_status st = tim::validate_logit_grads(hidden, w_vocab, tokens, T, d, V, temperature, lse, entropy,
+                                                  grad_logp, grad_entropy, dlogits, workspace, workspace_bytes);
+  if (st != TIM_OK || T == 0) return st;
+  tim_status r = hip_status(tim::launch_grad_coef(lse, entropy, grad_logp, grad_entropy, tokens, T, V, temperature,
+                                                  workspace, stream));
+  if (r != TIM_OK) return r;
+  tim::DlogitsArgs a;
+  a.hidden = hidden;
+  a.w = w_vocab;
+  a.tokens = tokens;
+  a.coef = workspace;
+  a.rows = T;
+  a.d = d;
+  a.V = V;
+  a.inv_tau = inv_temperature(temperature);
+  a.dacc = dlogits;
+  a.ld = (int64_t)tim::n_tiles_of(V) * TIM_VOCAB_TILE;
+  return hip_status(tim::launch_dlogits(a, stream));
+}
+
+tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,
+                                 int32_t d, int32_t V, float temperature, const float* lse, const float* entropy,
+                                 const float* grad_logp, const float* grad_entropy, int64_t micro_batch,
+                                 float* grad_hidden, float* grad_w, int32_t accumulate_grad_w, void* workspace,
+                                 size_t workspace_bytes, hipStream_t stream) {
+  tim_status st = tim::validate_backward(hidden, w_vocab, tokens, T, d, V, temperature, lse, entropy, grad_logp,
+                                         grad_entropy, micro_batch, grad_hidden, grad_w, accumulate_grad_w,
+                                         workspace, workspace_bytes);
+  if (st != TIM_OK) return st;
+  if (!grad_hidden && !grad_w) return TIM_OK;
+  if (T == 0) {  // no tokens: dW is zero unless it accumulates
+    if (grad_w && !accumulate_grad_w) return hip_status(tim::launch_fill_zero(grad_w, (int64_t)V * d, stream));
+    return TIM_OK;
+  }
+  const tim::BackwardLayout l = tim::backward_layout(T, d, V, micro_batch);
+  unsigned char* ws = (unsigned char*)workspace;
+  void* coef = ws + l.coef;
+  void* wt = ws + l.wt;
+  void* dacc = ws + l.dacc;
+  void* dacct = ws + l.dacct;
+  void* ht = ws + l.ht;
+  const float inv_tau = inv_temperature(temperature);
+  const __bf16* h = (const __bf16*)hidden;
+
+  if (grad_hidden) {  // W^T [d, V_pad], zero columns past V
+    st = hip_status(tim::launch_transpose(w_vocab, V, d, d, wt, l.v_pad, l.v_pad, stream));
+    if (st != TIM_OK) return st;
+  }
+  for (int64_t t0 = 0; t0 < T; t0 += l.step) {
+    const int64_t rows = (T - t0) < l.step ? (T - t0) : l.step;
+    const int64_t t_pad = tim::round_up(rows, 128);
+    st = hip_status(tim::launch_grad_coef(lse + t0, entropy ? entropy + t0 : nullptr, grad_logp + t0,
+                                          grad_entropy ? grad_entropy + t0 : nullptr, tokens + t0, rows, V,
+                                          temperature, coef, stream));
+    if (st != TIM_OK) return st;
+    tim::DlogitsArgs a;
+    a.hidden = h + t0 * d;
+    a.w = w_vocab;
+    a.tokens = tokens + t0;
+    a.coef = coef;
+    a.rows = rows;
+    a.d = d;
+    a.V = V;
+    a.inv_tau = inv_tau;
+    a.dacc = dacc;
+    a.ld = l.v_pad;
+    st = hip_status(tim::launch_dlogits(a, stream));
+    if (st != TIM_OK) return st;
+    if (grad_hidden) {  // dh = dlogits . W over the padded vocabulary
+      tim::GemmArgs g;
+      g.a = wt;
+      g.b = dacc;
+      g.b_rows = rows;
+      g.a_rows = d;
+      g.K = (int32_t)l.v_pad;
+      g.out = grad_hidden + t0 * d;
+      g.ldo = d;
+      g.accumulate = 0;
+      st = hip_status(tim::launch_gemm(g, stream));
+      if (st != TIM_OK) return st;
+    }
+    if (grad_w) {  // dW (+)= dlogits^T . h over this micro-batch's tokens
+      st = hip_status(tim::launch_transpose(dacc, rows, l.v_pad, l.v_pad, dacct, t_pad, t_pad, stream));
+      if (st != TIM_OK) return st;
+      st = hip_status(tim::launch_transpose(h + t0 * d, rows, d, d, ht, t_pad, t_pad, stream));
+      if (st != TIM_OK) return st;
+      tim::GemmArgs g;
+      g.a = ht;
+      g.b = dacct;
+      g.b_rows = V;
+      g.a_rows = d;
+      g.K = (int32_t)t_pad;
+      g.out = grad_w;
+      g.ldo = d;
+      g.accumulate = (accumulate_grad_w || t0 > 0) ? 1 : 0;
+      st = hip_status(tim::launch_gemm(g, stream));
+      if (st != TIM_OK) return st;
+    }
+  }
+  return TIM_OK;
+}
+
 const char* tim_status_string(tim_status s) {
   switch (s) {
     case TIM_OK: return "TIM_OK";

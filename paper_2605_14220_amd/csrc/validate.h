@@ -86,4 +86,92 @@ inline tim_status validate_logits(const void* hidden, const void* w, int64_t T, 
   return TIM_OK;
 }
 
+// ------------------------------------------------------------ backward
+
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline size_t align256(size_t x) { return (x + 255u) & ~(size_t)255u; }
+
+// micro_batch of the backward: 0 (all T in one pass) or a positive multiple
+// of 128 tokens, so that micro-batches continue the weight-gradient chain on
+// whole MFMA k-steps.
+inline bool valid_backward_micro_batch(int64_t mb) { return mb == 0 || (mb > 0 && mb % 128 == 0); }
+
+// Largest token count of one backward pass: the weight-gradient operands of a
+// 256-row tile then stay within 32-bit buffer offsets.
+constexpr int64_t kMaxBackwardStep = (int64_t)1 << 22;
+
+// Workspace of tim_logprobs_backward, each part 256-byte aligned:
+// row words [step] float4 | W^T bf16 [d, V_pad] | dlogits bf16 [step, V_pad]
+// | dlogits^T bf16 [V_pad, T_pad] | hidden^T bf16 [d, T_pad].
+struct BackwardLayout {
+  int64_t step, t_pad, v_pad;
+  size_t coef, wt, dacc, dacct, ht, total;
+};
+
+inline BackwardLayout backward_layout(int64_t T, int32_t d, int32_t V, int64_t micro_batch) {
+  BackwardLayout l;
+  l.step = (micro_batch > 0 && micro_batch < T) ? micro_batch : T;
+  l.t_pad = round_up(l.step, 128);
+  l.v_pad = (int64_t)n_tiles_of(V) * TIM_VOCAB_TILE;
+  size_t off = 0;
+  l.coef = off;
+  off += align256((size_t)l.step * 16u);
+  l.wt = off;
+  off += align256((size_t)d * (size_t)l.v_pad * 2u);
+  l.dacc = off;
+  off += align256((size_t)l.step * (size_t)l.v_pad * 2u);
+  l.dacct = off;
+  off += align256((size_t)l.v_pad * (size_t)l.t_pad * 2u);
+  l.ht = off;
+  off += align256((size_t)d * (size_t)l.t_pad * 2u);
+  l.total = off;
+  return l;
+}
+
+// Arguments common to the logit-gradient pass and the full backward.
+inline tim_status validate_grad_inputs(const void* hidden, const void* w, const int32_t* tokens, float temperature,
+                                       const float* lse, const float* entropy, const float* grad_logp,
+                                       const float* grad_entropy) {
+  if (!hidden || !w || !tokens || !lse || !grad_logp) return TIM_ERR_NULL;
+  if (grad_entropy && !entropy) return TIM_ERR_NULL;
+  if (!positive_finite(temperature)) return TIM_ERR_VALUE;
+  if (!aligned16(hidden) || !aligned16(w)) return TIM_ERR_VALUE;
+  return TIM_OK;
+}
+
+inline tim_status validate_backward(const void* hidden, const void* w, const int32_t* tokens, int64_t T,
+                                    int32_t d, int32_t V, float temperature, const float* lse,
+                                    const float* entropy, const float* grad_logp, const float* grad_entropy,
+                                    int64_t micro_batch, const float* grad_hidden, const float* grad_w,
+                                    int32_t accumulate, const void* ws, size_t ws_bytes) {
+  if (T < 0) return TIM_ERR_SHAPE;
+  const tim_status s = check_shape(T, d, V, TIM_ORDER_INVARIANT);
+  if (s != TIM_OK) return s;
+  if (!positive_finite(temperature)) return TIM_ERR_VALUE;
+  if (!valid_backward_micro_batch(micro_batch) || (accumulate != 0 && accumulate != 1)) return TIM_ERR_VALUE;
+  if ((grad_hidden && !aligned16(grad_hidden)) || (grad_w && !aligned16(grad_w))) return TIM_ERR_VALUE;
+  if (T == 0 || (!grad_hidden && !grad_w)) return TIM_OK;
+  if (backward_layout(T, d, V, micro_batch).step > kMaxBackwardStep) return TIM_ERR_VALUE;
+  const tim_status g = validate_grad_inputs(hidden, w, tokens, temperature, lse, entropy, grad_logp, grad_entropy);
+  if (g != TIM_OK) return g;
+  if (!ws || !aligned16(ws) || ws_bytes < backward_layout(T, d, V, micro_batch).total) return TIM_ERR_WORKSPACE;
+  return TIM_OK;
+}
+
+inline tim_status validate_logit_grads(const void* hidden, const void* w, const int32_t* tokens, int64_t T,
+                                       int32_t d, int32_t V, float temperature, const float* lse,
+                                       const float* entropy, const float* grad_logp, const float* grad_entropy,
+                                       const void* dlogits, const void* ws, size_t ws_bytes) {
+  if (T < 0) return TIM_ERR_SHAPE;
+  const tim_status s = check_shape(T, d, V, TIM_ORDER_INVARIANT);
+  if (s != TIM_OK) return s;
+  if (T == 0) return TIM_OK;
+  if (!dlogits) return TIM_ERR_NULL;
+  const tim_status g = validate_grad_inputs(hidden, w, tokens, temperature, lse, entropy, grad_logp, grad_entropy);
+  if (g != TIM_OK) return g;
+  if (!aligned16(dlogits)) return TIM_ERR_VALUE;
+  if (!ws || !aligned16(ws) || ws_bytes < (size_t)T * 16u) return TIM_ERR_WORKSPACE;
+  return TIM_OK;
+}
+
 }  // namespace tim

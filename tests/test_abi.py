@@ -37,7 +37,8 @@ def lib():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    assert names == ["tim_logits", "tim_logprobs", "tim_logprobs_merge", "tim_logprobs_partials",
+    assert names == ["tim_logit_grads", "tim_logits", "tim_logprobs", "tim_logprobs_backward",
+                     "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_partials",
                      "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_status_string"]
 
 
@@ -249,3 +250,98 @@ def test_python_binding_rejects_cpu_tensors():
         tim.logprobs(h, w, tok.long())
     with pytest.raises(ValueError, match="GPU"):
         tim.mismatch(torch.zeros(3), torch.zeros(3))
+
+
+# ---------------------------------------------------------------- backward
+
+def _bwd_size(T, d, V, mb):
+    step = mb if 0 < mb < T else T
+    t_pad = -(-step // 128) * 128
+    v_pad = -(-V // 256) * 256
+    a = lambda x: -(-x // 256) * 256
+    return a(step * 16) + a(2 * d * v_pad) + a(2 * step * v_pad) + a(2 * v_pad * t_pad) + a(2 * d * t_pad)
+
+
+@pytest.mark.parametrize("T,d,V,mb", [(700, 256, 4173, 128), (138564, 4096, 151936, 16384), (1, 128, 1, 0),
+                                      (300, 640, 5000, 0), (300, 640, 5000, 1024)])
+def test_backward_workspace_size_formula(lib, T, d, V, mb):
+    assert tim.backward_workspace_size(T, d, V, mb) == _bwd_size(T, d, V, mb)
+
+
+@pytest.mark.parametrize("args", [(0, 256, 4096, 0), (-1, 256, 4096, 0), (10, 100, 4096, 0), (10, 256, 0, 0),
+                                  (10, 256, 4096, 100), (10, 256, 4096, -128), (2 ** 22 + 1, 128, 256, 0),
+                                  (10, 256, 2048 * 256 + 1, 0)])
+def test_backward_workspace_size_zero_when_invalid(lib, args):
+    assert lib.tim_logprobs_backward_workspace_size(*args) == 0
+
+
+def _bwd(lib, **kw):
+    g = lambda k, v: kw.get(k, v)
+    T, d, V, mb = g("T", 8), g("d", 256), g("V", 4096), g("mb", 0)
+    ws_bytes = g("ws_bytes", _bwd_size(max(T, 1), d, V, mb))
+    return lib.tim_logprobs_backward(g("hidden", FAKE), g("w", FAKE), g("tokens", FAKE), T, d, V, g("tau", 1.0),
+                                     g("lse", FAKE), g("ent", FAKE), g("gl", FAKE), g("ge", FAKE), mb,
+                                     g("gh", FAKE), g("gw", FAKE), g("acc", 0), g("ws", FAKE), ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(d=100), Status.ERR_SHAPE),
+    (dict(d=0), Status.ERR_SHAPE),
+    (dict(V=0), Status.ERR_SHAPE),
+    (dict(V=2048 * 256 + 1), Status.ERR_SHAPE),
+    (dict(tau=0.0), Status.ERR_VALUE),
+    (dict(tau=math.nan), Status.ERR_VALUE),
+    (dict(mb=100), Status.ERR_VALUE),
+    (dict(mb=-128), Status.ERR_VALUE),
+    (dict(acc=2), Status.ERR_VALUE),
+    (dict(gh=FAKE_MIS), Status.ERR_VALUE),
+    (dict(gw=FAKE_MIS), Status.ERR_VALUE),
+    (dict(T=2 ** 22 + 1, d=128, V=256), Status.ERR_VALUE),
+    (dict(hidden=None), Status.ERR_NULL),
+    (dict(w=None), Status.ERR_NULL),
+    (dict(tokens=None), Status.ERR_NULL),
+    (dict(lse=None), Status.ERR_NULL),
+    (dict(gl=None), Status.ERR_NULL),
+    (dict(ent=None), Status.ERR_NULL),          # grad_entropy given without entropy
+    (dict(hidden=FAKE_MIS), Status.ERR_VALUE),
+    (dict(w=FAKE_MIS), Status.ERR_VALUE),
+    (dict(ws=None), Status.ERR_WORKSPACE),
+    (dict(ws=FAKE_MIS), Status.ERR_WORKSPACE),
+    (dict(ws_bytes=100), Status.ERR_WORKSPACE),
+])
+def test_backward_rejects(lib, kw, expect):
+    assert _bwd(lib, **kw) == expect
+
+
+def test_backward_noops(lib):
+    # no outputs requested: validated, nothing enqueued (inputs never read)
+    assert _bwd(lib, gh=None, gw=None, hidden=None, lse=None, ws=None) == Status.OK
+    # T == 0 without a weight gradient to clear
+    assert _bwd(lib, T=0, gw=None, hidden=None, ws=None) == Status.OK
+    assert _bwd(lib, T=0, acc=1, hidden=None, ws=None) == Status.OK
+    # entropy may be NULL when grad_entropy is
+    assert _bwd(lib, ent=None, ge=None, gh=None, gw=None) == Status.OK
+
+
+def _lg(lib, **kw):
+    g = lambda k, v: kw.get(k, v)
+    T = g("T", 8)
+    return lib.tim_logit_grads(g("hidden", FAKE), g("w", FAKE), g("tokens", FAKE), T, g("d", 256), g("V", 4096),
+                               g("tau", 1.0), g("lse", FAKE), g("ent", FAKE), g("gl", FAKE), g("ge", FAKE),
+                               g("out", FAKE), g("ws", FAKE), g("ws_bytes", 16 * max(T, 1)), None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(d=200), Status.ERR_SHAPE),
+    (dict(out=None), Status.ERR_NULL),
+    (dict(lse=None), Status.ERR_NULL),
+    (dict(ent=None), Status.ERR_NULL),
+    (dict(out=FAKE_MIS), Status.ERR_VALUE),
+    (dict(tau=-1.0), Status.ERR_VALUE),
+    (dict(ws_bytes=16 * 8 - 1), Status.ERR_WORKSPACE),
+])
+def test_logit_grads_rejects(lib, kw, expect):
+    assert _lg(lib, **kw) == expect
+    assert _lg(lib, T=0, out=None, hidden=None) == Status.OK
