@@ -12,6 +12,10 @@ temperature + per-tile softmax partials + token gather) and the merge kernel
 the stream against a second engine's log-probs (computed once, untimed, by the
 split-K4 reduction order).
 
+Reported beside the step (not part of `value`): rollout decode batches, the
+sequence-level statistics, and the backward of the fused log-prob over the
+same stream (logit gradients, grad_hidden, grad_w).
+
 Prints ONE JSON line on stdout; progress goes to stderr.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--config mid]
@@ -40,8 +44,11 @@ def log(*a):
 
 
 def kernel_source_hash() -> str:
-    p = os.path.join(ROOT, "paper_2605_14220_amd", "csrc", "lmhead.hip")
-    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+    """Hash of the sources of the LM-head forward kernel (its tile pass and epilogue)."""
+    h = hashlib.sha256()
+    for f in ("tilepass.h", "lmhead.hip"):
+        h.update(open(os.path.join(ROOT, "paper_2605_14220_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(name: str):
@@ -95,6 +102,8 @@ def main(argv=None):
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after timing, run a plain copy kernel of known size (torch.neg over 2^28 fp32: "
                          "1 GiB read + 1 GiB written) so a counter profile can scale HBM byte counters")
+    ap.add_argument("--no-backward", dest="backward", action="store_false",
+                    help="skip the backward measurement")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path runs on a single GPU, "
@@ -252,6 +261,40 @@ def main(argv=None):
            "max_k3_score": float(seq_out[0].max().item())}
     log(f"[bench] sequence-level K3 scores / mask / weights over {len(lens)} responses: {seq_ms * 1e3:.1f} us/call")
 
+    # backward of the fused log-prob over the whole stream (the trainer's gradients)
+    bwd = None
+    if args.backward:
+        g = torch.Generator(device="cpu").manual_seed(99)
+        g_lp = torch.randn(T, generator=g).to(dev)
+        g_h = (0.1 * torch.randn(T, generator=g)).to(dev)
+        bws = torch.empty(tim.backward_workspace_size(T, d, V, mb), dtype=torch.uint8, device=dev)
+        gw = torch.empty((V, d), dtype=torch.float32, device=dev)
+
+        def bstep():
+            return tim.logprobs_backward(h, W, tok, lse, g_lp, tau, entropy=ent, grad_entropy=g_h, micro_batch=mb,
+                                         grad_w=gw, workspace=bws)
+        gh, _ = bstep()
+        torch.cuda.synchronize()
+        b0 = torch.cuda.Event(enable_timing=True)
+        b1 = torch.cuda.Event(enable_timing=True)
+        n_b = 2
+        b0.record(stream)
+        for _ in range(n_b):
+            gh, _ = bstep()
+        b1.record(stream)
+        torch.cuda.synchronize()
+        b_ms = b0.elapsed_time(b1) / n_b
+        b_flop = 3 * 2.0 * d * V * T
+        bwd = {"ms_per_call": b_ms, "tokens_per_s": T / (b_ms / 1e3), "bound": "mfma",
+               "achieved": b_flop / (b_ms / 1e3) / 1e12, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+               "frac": b_flop / (b_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, "flop_per_call": b_flop,
+               "micro_batch": mb, "workspace_GB": bws.numel() / 1e9,
+               "finite": bool(torch.isfinite(gh).all().item() and torch.isfinite(gw).all().item())}
+        log(f"[bench] backward over {T} tokens (micro-batch {mb}): {b_ms:.1f} ms/call, {bwd['tokens_per_s']:,.0f} "
+            f"tokens/s, {bwd['achieved']:.1f} TFLOP/s = {bwd['frac']:.1%} of bf16 peak (3 contractions)")
+        del bws, gw, gh
+        torch.cuda.empty_cache()
+
     # mismatch report between the two engines (context)
     dl = stats[0].abs()
     q = torch.quantile(dl.float(), torch.tensor([0.5, 0.99], device=dev)).tolist()
@@ -300,6 +343,7 @@ def main(argv=None):
         "mismatch_vs_splitk4": mis,
         "rollout_decode": rollout,
         "sequence_mismatch": seq,
+        "backward": bwd,
     }
     print(json.dumps(out), flush=True)
 

@@ -87,6 +87,47 @@ def test_mid_micro_batches():
     assert abs(H.double().mean().item() - (math.log(cfg.V) - sig2 / 2)) < 0.05
 
 
+def test_mid_backward():
+    """The backward at the mid shape (d=4096, V=151936) on the first 20000 tokens
+    (a full 16384-token micro-batch and a ragged one): sampled grad_hidden rows
+    against the oracle within the derived bound, grad_hidden and grad_w bitwise
+    across micro-batch sizes, and sum_v grad_w[v, :] = 0 within its bound."""
+    cfg, h, W, tok = workload("mid")
+    T, d, V, tau = 20000, cfg.d, cfg.V, cfg.temperature
+    hs, ts = h[:T].contiguous(), tok[:T].contiguous()
+    _, H, lse = tim.logprobs(hs, W, ts, tau, micro_batch=16384, lse=True)
+    g = torch.Generator(device="cpu").manual_seed(99)
+    gl = torch.randn(T, generator=g).cuda()
+    ge = (0.1 * torch.randn(T, generator=g)).cuda()
+    gh, gw = tim.logprobs_backward(hs, W, ts, lse, gl, tau, entropy=H, grad_entropy=ge, micro_batch=16384)
+    gh2, gw2 = tim.logprobs_backward(hs, W, ts, lse, gl, tau, entropy=H, grad_entropy=ge, micro_batch=4096)
+    assert bits_equal(gh, gh2) and bits_equal(gw, gw2)
+    torch.cuda.synchronize()
+    wf = oracle.bf16_to_f64(bf16_bits(W))
+    v_pad = (V + 255) // 256 * 256
+    c = 2.0 ** -8 + (v_pad / 32 + 64) * 2.0 ** -24
+    rows = np.sort(np.random.default_rng(3).choice(T, size=4, replace=False))
+    worst = 0.0
+    for r in rows:
+        dacc = oracle.logit_grads(bf16_bits(hs[r:r + 1]), bf16_bits(W), ts[r:r + 1].cpu().numpy(), tau,
+                                  gl[r:r + 1].double().cpu().numpy(), ge[r:r + 1].double().cpu().numpy())
+        ref = (dacc @ wf)[0]
+        mag = (np.abs(dacc) @ np.abs(wf))[0]
+        err = np.abs(gh[r].double().cpu().numpy() - ref)
+        worst = max(worst, float((err / (c * mag + 1e-5 * mag.max())).max()))
+    print(f"[parity] mid grad_hidden on {len(rows)} sampled rows: max err/bound = {worst:.3f}")
+    assert worst <= 1.0
+    # sum_v dlogits = 0 per row: |sum_v grad_w[v, k]| <= c_w sum_t sum_v |dlogits| |h_tk|, and
+    # sum_v |dlogits_tv| <= (2 |g_t| + 2 |e_t| log V) / tau (sum_v p |q + H| <= 2 H <= 2 log V)
+    cw = 2.0 ** -8 + ((T + 127) // 128 * 128 / 32 + 64) * 2.0 ** -24
+    row_l1 = (2 * gl.double().abs() + 2 * ge.double().abs() * math.log(V)) / tau
+    bound = cw * (row_l1[:, None] * hs.double().abs()).sum(dim=0)
+    colsum = gw.double().sum(dim=0).abs()
+    print(f"[invariant] mid: max |sum_v grad_w| / bound = {(colsum / bound).max().item():.2e}")
+    assert (colsum <= bound).all()
+    assert torch.isfinite(gw).all()
+
+
 def test_stress_invariance_and_mismatch_report():
     cfg, h, W, tok = workload("stress")
     T = h.shape[0]
