@@ -539,3 +539,117 @@ def test_grads_linear_in_upstream():
     np.testing.assert_allclose(c, 2 * a - b, atol=1e-14)
     z = oracle.logit_grads(hb, wb, tok, 1.3, np.zeros(T), np.zeros(T))
     np.testing.assert_array_equal(z, 0.0)
+
+
+# ---------------------------------------------------------------- final RMS norm
+
+def test_round_bf16_matches_torch_cast_of_fp32_values():
+    rng = np.random.default_rng(20)
+    v = (rng.standard_normal(200000) * np.exp(rng.uniform(-20, 20, 200000))).astype(np.float32)
+    got = oracle.round_bf16(v.astype(np.float64))
+    ref = torch.as_tensor(v).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_round_bf16_ties_to_even_and_off_tie():
+    u = 2.0 ** -7  # bf16 spacing in [1, 2)
+    cases = [(1 + u / 2, 1.0), (1 + 3 * u / 2, 1 + 2 * u), (-(1 + u / 2), -1.0), (1 + u / 2 + 2.0 ** -40, 1 + u),
+             (1 + u / 2 - 2.0 ** -40, 1.0), (0.0, 0.0), (2 - u / 4, 2.0), (2 - 3 * u / 4, 2 - u), (2 - u / 2, 2.0),
+             (3 * 2.0 ** -130, None)]
+    for v, want in cases:
+        got = float(oracle.round_bf16(np.array([v]))[0])
+        if want is None:  # below bf16's normal range: still a multiple of its own 8-bit spacing
+            m, e = math.frexp(got)
+            assert m * 256 == int(m * 256)
+        else:
+            assert got == want, (v, got, want)
+
+
+def test_rmsnorm_constant_row_closed_form():
+    T, d = 3, 64
+    c = np.array([0.5, -3.0, 0.0078125])
+    x = np.repeat(c[:, None], d, axis=1)
+    for eps in (0.0, 1e-6):
+        hb, r, n = oracle.rmsnorm(_bits(x), None, eps)
+        for t in range(T):
+            assert r[t] == 1.0 / math.sqrt(c[t] * c[t] + eps)
+            np.testing.assert_array_equal(n[t], c[t] * r[t])
+        np.testing.assert_array_equal(oracle.bf16_to_f64(hb), oracle.round_bf16(n))
+
+
+@pytest.mark.parametrize("eps", [1e-6, 1e-2])
+def test_rmsnorm_matches_torch_rms_norm_float64(eps):
+    T, d = 9, 384
+    xb = _rand_bits((T, d), 21, 3.0)
+    gb = _rand_bits((d,), 22, 1.0)
+    x = torch.tensor(oracle.bf16_to_f64(xb))
+    g = torch.tensor(oracle.bf16_to_f64(gb))
+    _, r, n = oracle.rmsnorm(xb, gb, eps)
+    ref = torch.nn.functional.rms_norm(x, (d,), weight=None, eps=eps).numpy()
+    np.testing.assert_allclose(n, ref, rtol=1e-14, atol=0)
+    ref_g = torch.nn.functional.rms_norm(x, (d,), weight=g, eps=eps).numpy()
+    np.testing.assert_allclose(n * g.numpy()[None, :], ref_g, rtol=1e-14, atol=0)
+
+
+def test_rmsnorm_roundings_match_bf16_model_arithmetic():
+    """The model's own arithmetic, in torch on the CPU: fp32 variance and scale,
+    a cast to bf16, then bf16 * bf16 with the weight. It rounds from fp32 where
+    the oracle rounds from fp64, so the two agree except on rare straddles."""
+    T, d, eps = 64, 256, 1e-6
+    xb = _rand_bits((T, d), 23, 2.0)
+    gb = _rand_bits((d,), 24, 1.0)
+    hb, _, _ = oracle.rmsnorm(xb, gb, eps)
+    x32 = torch.tensor(oracle.bf16_to_f64(xb), dtype=torch.float32)
+    var = x32.pow(2).mean(-1, keepdim=True)
+    hs = (x32 * torch.rsqrt(var + eps)).to(torch.bfloat16)
+    g16 = torch.tensor(oracle.bf16_to_f64(gb), dtype=torch.float32).to(torch.bfloat16)
+    ref = bf16_bits(g16 * hs)
+    same = (hb == ref).mean()
+    assert same >= 0.999, same
+    # without a weight: the single rounding of the normalised row, and a weight of ones changes nothing
+    hb1, _, _ = oracle.rmsnorm(xb, None, eps)
+    hbo, _, _ = oracle.rmsnorm(xb, _bits(np.ones(d)), eps)
+    np.testing.assert_array_equal(hb1, hbo)
+    assert (hb1 == bf16_bits(hs)).mean() >= 0.999
+
+
+def test_rmsnorm_grads_match_finite_differences():
+    T, d, eps = 2, 8, 1e-3
+    xb, gb = _grid_bits((T, d), 25), _grid_bits((d,), 26)
+    G = np.random.default_rng(27).standard_normal((T, d))
+    dx, dg = oracle.rmsnorm_grads(xb, gb, eps, G)
+
+    def L_x(xbits):
+        return float((G * oracle.bf16_to_f64(gb)[None, :] * oracle.rmsnorm(xbits, gb, eps)[2]).sum())
+
+    def L_g(gbits):
+        return float((G * oracle.bf16_to_f64(gbits)[None, :] * oracle.rmsnorm(xb, gbits, eps)[2]).sum())
+    for t in range(T):
+        for k in range(d):
+            fd = _fd(L_x, xb, (t, k))
+            assert abs(fd - dx[t, k]) <= 1e-6 * (1 + abs(fd)), (t, k, fd, dx[t, k])
+    for k in range(d):
+        fd = _fd(L_g, gb, (k,))
+        assert abs(fd - dg[k]) <= 1e-9 * (1 + abs(fd)), (k, fd, dg[k])
+
+
+def test_rmsnorm_grads_match_torch_autograd_and_scale_identity():
+    T, d = 6, 96
+    xb = _rand_bits((T, d), 28, 2.0)
+    gb = _rand_bits((d,), 29, 1.0)
+    G = np.random.default_rng(30).standard_normal((T, d))
+    for eps in (1e-6, 0.0):
+        x = torch.tensor(oracle.bf16_to_f64(xb), requires_grad=True)
+        g = torch.tensor(oracle.bf16_to_f64(gb), requires_grad=True)
+        (torch.nn.functional.rms_norm(x, (d,), weight=g, eps=eps) * torch.tensor(G)).sum().backward()
+        dx, dg = oracle.rmsnorm_grads(xb, gb, eps, G)
+        np.testing.assert_allclose(dx, x.grad.numpy(), rtol=1e-11, atol=1e-13)
+        np.testing.assert_allclose(dg, g.grad.numpy(), rtol=1e-11, atol=1e-13)
+    # eps = 0: the normalised row does not change with the row's scale, so x . dL/dx = 0 per row
+    dx0, _ = oracle.rmsnorm_grads(xb, gb, 0.0, G)
+    x0 = oracle.bf16_to_f64(xb)
+    np.testing.assert_allclose((x0 * dx0).sum(axis=1), 0.0, atol=1e-12)
+    # without a weight: the same as a weight of ones
+    a = oracle.rmsnorm_grads(xb, None, 1e-6, G)
+    b = oracle.rmsnorm_grads(xb, _bits(np.ones(d)), 1e-6, G)
+    np.testing.assert_array_equal(a[0], b[0])

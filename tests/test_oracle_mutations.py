@@ -42,6 +42,14 @@ MUTATIONS = [
     ("grads.py", "gb = np.where(ok, g[r0:r1], 0.0)", "gb = g[r0:r1]"),
     ("grads.py", "dw = dacc.T @ h", "dw = dacc.T @ h[::-1]"),
     ("grads.py", "dh = dacc @ w", "dh = dacc @ w[::-1]"),
+    ("rmsnorm.py", "np.rint(m * 256.0)", "np.floor(m * 256.0 + 0.5)"),
+    ("rmsnorm.py", "np.rint(m * 256.0) / 256.0", "np.rint(m * 128.0) / 128.0"),
+    ("rmsnorm.py", "(x * x).sum(axis=1) / d + float(eps))", "(x * x).sum(axis=1) + float(eps))"),
+    ("rmsnorm.py", "[None, :] * h)", "[None, :] * n)"),
+    ("rmsnorm.py", "G - (r ** 3 * s / d)", "G + (r ** 3 * s / d)"),
+    ("rmsnorm.py", "(r ** 3 * s / d)", "(r ** 2 * s / d)"),
+    ("rmsnorm.py", "s = (G * g[None, :] * x)", "s = (G * x)"),
+    ("rmsnorm.py", "dg = (G * x * r[:, None])", "dg = (G * x)"),
 ]
 
 
