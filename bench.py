@@ -261,6 +261,42 @@ def main(argv=None):
            "max_k3_score": float(seq_out[0].max().item())}
     log(f"[bench] sequence-level K3 scores / mask / weights over {len(lens)} responses: {seq_ms * 1e3:.1f} us/call")
 
+    # the final RMS norm in front of the head over the whole stream (HBM-bound), and its backward
+    gam = (1.0 + 0.1 * torch.randn(d, generator=torch.Generator(device="cpu").manual_seed(98))).to(torch.bfloat16).to(dev)
+    h_n = torch.empty_like(h)
+    for _ in range(2):
+        tim.rmsnorm(h, gam, 1e-6, out=h_n)
+    n0 = torch.cuda.Event(enable_timing=True)
+    n1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    n0.record(stream)
+    for _ in range(10):
+        _, rstd_n = tim.rmsnorm(h, gam, 1e-6, out=h_n)
+    n1.record(stream)
+    torch.cuda.synchronize()
+    nf_ms = n0.elapsed_time(n1) / 10
+    G_n = torch.randn(T, d, generator=torch.Generator(device=dev).manual_seed(97), device=dev)
+    gg_n = torch.empty(d, dtype=torch.float32, device=dev)
+    gx_n, _ = tim.rmsnorm_backward(h, gam, rstd_n, G_n, grad_gamma=gg_n)
+    torch.cuda.synchronize()
+    n0.record(stream)
+    for _ in range(5):
+        tim.rmsnorm_backward(h, gam, rstd_n, G_n, grad_gamma=gg_n)
+    n1.record(stream)
+    torch.cuda.synchronize()
+    nb_ms = n0.elapsed_time(n1) / 5
+    nf_bytes = 4.0 * T * d + 4.0 * T
+    nb_bytes = 16.0 * T * d
+    norm = {"forward_ms": nf_ms, "forward_GBps": nf_bytes / (nf_ms / 1e3) / 1e9,
+            "forward_frac": nf_bytes / (nf_ms / 1e3) / 1e9 / PEAK_HBM_GBS, "forward_bytes": nf_bytes,
+            "backward_ms": nb_ms, "backward_GBps": nb_bytes / (nb_ms / 1e3) / 1e9,
+            "backward_frac": nb_bytes / (nb_ms / 1e3) / 1e9 / PEAK_HBM_GBS, "backward_bytes": nb_bytes,
+            "bound": "hbm", "peak_GBps": PEAK_HBM_GBS}
+    log(f"[bench] final RMS norm over {T} rows: forward {nf_ms:.3f} ms ({norm['forward_GBps']:.0f} GB/s = "
+        f"{norm['forward_frac']:.1%} of 8 TB/s), backward {nb_ms:.3f} ms ({norm['backward_GBps']:.0f} GB/s algorithmic)")
+    del G_n, gx_n, h_n
+    torch.cuda.empty_cache()
+
     # backward of the fused log-prob over the whole stream (the trainer's gradients)
     bwd = None
     if args.backward:
@@ -344,6 +380,7 @@ def main(argv=None):
         "rollout_decode": rollout,
         "sequence_mismatch": seq,
         "backward": bwd,
+        "rmsnorm": norm,
     }
     print(json.dumps(out), flush=True)
 

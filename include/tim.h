@@ -246,6 +246,42 @@ tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_
                            const float* grad_logp, const float* grad_entropy,
                            void* dlogits, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Final RMS normalisation in front of the LM head (Section 3.1 lists RMSNorm
+ * among the batch-invariant kernels; root-mean-square layer normalisation).
+ * Row t of x (bf16 [T, d] row-major, 16-byte aligned, d a multiple of 8):
+ *   rstd[t] = 1 / sqrt(mean_k x[t,k]^2 + eps)                       (fp32)
+ *   h[t,k]  = bf16(gamma[k] * bf16(x[t,k] * rstd[t]))              (bf16(x * rstd) if gamma is NULL)
+ * rounding to nearest even, the arithmetic of the model implementation the
+ * engine follows (fp32 scale, a cast to bf16, a bf16 multiply by the weight).
+ * The sum of squares is reduced in one fixed order that depends only on d, so
+ * a row's outputs are bitwise independent of T and of its position. h (bf16
+ * [T, d], 16-byte aligned) feeds tim_logprobs as `hidden`; rstd (fp32 [T], may
+ * be NULL) feeds the backward. gamma bf16 [d], 16-byte aligned, or NULL.
+ * eps finite and >= 0. Errors: TIM_ERR_SHAPE for T < 0, T > 65535 * 256 or a
+ * bad d; TIM_ERR_VALUE for a bad eps or alignment; TIM_ERR_NULL for a NULL x
+ * or h with T > 0. */
+tim_status tim_rmsnorm(const void* x, const void* gamma, int64_t T, int32_t d, float eps,
+                       void* h, float* rstd, hipStream_t stream);
+
+/* Backward of tim_rmsnorm with the bf16 casts passed straight through, for
+ * grad_h = dL/dh (fp32 [T, d], 16-byte aligned; tim_logprobs_backward's
+ * grad_hidden) and rstd from the forward:
+ *   grad_x[t,k]  = rstd g_k G_tk - (rstd^3 / d) x_tk sum_j G_tj g_j x_tj    (fp32 [T, d])
+ *   grad_gamma[k] (+)= sum_t G_tk x_tk rstd_t                                (fp32 [d])
+ * (g = gamma, or ones when NULL). grad_x's row sum runs in the forward's
+ * fixed order (batch-invariant); grad_gamma sums blocks of 256 rows in row
+ * order, then the blocks in order: deterministic, no atomics. Either output may
+ * be NULL (not computed); with accumulate_grad_gamma = 1 the result is added
+ * to grad_gamma's contents. The workspace holds
+ * tim_rmsnorm_backward_workspace_size(T, d) = ceil(T / 256) * d * 4 bytes
+ * (needed only for grad_gamma). Errors as tim_rmsnorm; TIM_ERR_WORKSPACE for a
+ * missing or small workspace. */
+size_t tim_rmsnorm_backward_workspace_size(int64_t T, int32_t d);
+tim_status tim_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
+                                int64_t T, int32_t d, float* grad_x, float* grad_gamma,
+                                int32_t accumulate_grad_gamma, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
 /* Test and debugging aid: writes the fp32 logits z[T, V] (row-major) exactly as
  * tim_logprobs forms them before the softmax (same kernel code, same
  * accumulation order, same temperature multiply), for checking the gather and

@@ -93,6 +93,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tim_logit_grads.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
                                     c.c_float, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p,
                                     c.c_void_p, c.c_size_t, c.c_void_p]
+    lib.tim_rmsnorm.restype = c.c_int
+    lib.tim_rmsnorm.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_float, c.c_void_p, c.c_void_p,
+                                c.c_void_p]
+    lib.tim_rmsnorm_backward_workspace_size.restype = c.c_size_t
+    lib.tim_rmsnorm_backward_workspace_size.argtypes = [c.c_int64, c.c_int32]
+    lib.tim_rmsnorm_backward.restype = c.c_int
+    lib.tim_rmsnorm_backward.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32,
+                                         c.c_void_p, c.c_void_p, c.c_int32, c.c_void_p, c.c_size_t, c.c_void_p]
     lib.tim_logits.restype = c.c_int
     lib.tim_logits.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32, c.c_float,
                                c.c_int32, c.c_void_p, c.c_void_p]
@@ -327,3 +335,49 @@ def logit_grads(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tenso
                                _ptr(entropy), _ptr(grad_logp), _ptr(grad_entropy), _ptr(out), _ptr(ws),
                                ws.numel(), _stream(dev)))
     return out
+
+
+def rmsnorm(x: torch.Tensor, gamma: torch.Tensor | None = None, eps: float = 1e-6, out: torch.Tensor | None = None):
+    """Final RMS norm: (h bf16 [T, d], rstd fp32 [T]) of x bf16 [T, d] (see include/tim.h)."""
+    lib = load_library()
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or (gamma is not None and gamma.dtype != torch.bfloat16):
+        raise TypeError("tim.rmsnorm: x must be bf16 [T, d] and gamma bf16 [d]")
+    T, d = x.shape
+    if gamma is not None and gamma.shape != (d,):
+        raise ValueError("tim.rmsnorm: gamma must be [d]")
+    _require_gpu(x, gamma, out)
+    h = torch.empty_like(x) if out is None else out
+    rstd = torch.empty(T, dtype=torch.float32, device=x.device)
+    _check(lib.tim_rmsnorm(_ptr(x), _ptr(gamma), T, d, float(eps), _ptr(h), _ptr(rstd), _stream(x.device)))
+    return h, rstd
+
+
+def rmsnorm_backward(x: torch.Tensor, gamma: torch.Tensor | None, rstd: torch.Tensor, grad_h: torch.Tensor,
+                     want_x: bool = True, want_gamma: bool = True, grad_gamma: torch.Tensor | None = None,
+                     accumulate: bool = False):
+    """(grad_x fp32 [T, d] or None, grad_gamma fp32 [d] or None) of the final RMS norm."""
+    lib = load_library()
+    T, d = x.shape
+    if grad_h.dtype != torch.float32 or grad_h.shape != (T, d) or rstd.shape != (T,):
+        raise ValueError("tim.rmsnorm_backward: grad_h fp32 [T, d] and rstd [T]")
+    _require_gpu(x, gamma, rstd, grad_h, grad_gamma)
+    dev = x.device
+    gx = torch.empty((T, d), dtype=torch.float32, device=dev) if want_x else None
+    if want_gamma and grad_gamma is None:
+        if accumulate:
+            raise ValueError("tim.rmsnorm_backward: accumulate needs the grad_gamma buffer")
+        grad_gamma = torch.empty(d, dtype=torch.float32, device=dev)
+    gg = grad_gamma if want_gamma else None
+    ws = torch.empty(max(int(lib.tim_rmsnorm_backward_workspace_size(T, d)), 16), dtype=torch.uint8, device=dev)
+    _check(lib.tim_rmsnorm_backward(_ptr(x), _ptr(gamma), _ptr(rstd), _ptr(grad_h), T, d, _ptr(gx), _ptr(gg),
+                                    1 if accumulate else 0, _ptr(ws), ws.numel(), _stream(dev)))
+    return gx, gg
+
+
+def logprobs_from_residual(x: torch.Tensor, gamma: torch.Tensor | None, w_vocab: torch.Tensor, tokens: torch.Tensor,
+                           eps: float = 1e-6, temperature: float = 1.0, **kw):
+    """The final norm followed by the LM-head log-probs: (logp, entropy, lse, h, rstd).
+    Two C-ABI calls on the same stream; keyword arguments go to logprobs()."""
+    h, rstd = rmsnorm(x, gamma, eps)
+    lp, ent, lse = logprobs(h, w_vocab, tokens, temperature, **kw)
+    return lp, ent, lse, h, rstd

@@ -83,6 +83,14 @@ hipError_t launch_grad_coef(const float* lse, const float* entropy, const float*
                             const float* grad_entropy, const int32_t* tokens, int64_t rows, int V,
                             float temperature, void* coef, hipStream_t s);
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s);
+// Final RMS norm, one wavefront per row: h (bf16 [T, d]) and rstd (fp32 [T], may be null).
+hipError_t launch_rmsnorm(const void* x, const void* gamma, int64_t T, int d, float eps, void* h, float* rstd,
+                          hipStream_t s);
+// Its backward: grad_x (fp32 [T, d]) and/or grad_gamma (fp32 [d]) from grad_h
+// (fp32 [T, d]); `part` holds ceil(T / 256) * d floats of column partial sums.
+hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
+                                   int64_t T, int d, float* grad_x, float* grad_gamma, int accumulate, float* part,
+                                   hipStream_t s);
 hipError_t launch_mismatch(const float* a, const float* b, int64_t n, float C,
                            float* log_ratio, float* k3, float* w, hipStream_t s);
 // Per-response score / keep and per-token weights of a packed stream (one

@@ -1,0 +1,204 @@
+// Final RMS normalisation in front of the LM head, batch-invariant, and its
+// backward (Section 3.1 lists RMSNorm among the batch-invariant kernels; the
+// norm is Zhang and Sennrich's root-mean-square layer normalisation).
+//
+// Forward, one wavefront per row, d a multiple of 8:
+//   r   = 1 / sqrt(mean_k x_k^2 + eps)                      fp32
+//   h_k = bf16(g_k * bf16(x_k * r))  (bf16(x_k * r) without a weight)
+// the arithmetic of the model implementation the engine follows: the row is
+// widened to fp32, scaled, rounded to bf16, then multiplied by the bf16 weight
+// and rounded again. Lane l takes the 8-element chunks l, l + 64, l + 128, ...
+// and sums their squares in that order (one fma chain); the 64 lane sums
+// combine in a fixed butterfly, so r depends only on the row and d.
+//
+// Backward, with G = dL/dh (fp32) and the casts passed straight through:
+//   dx_k = r g_k G_k - (r^3 s / d) x_k,   s = sum_j G_j g_j x_j   (one wavefront per row)
+//   dg_k = sum_t G_tk x_tk r_t   as fixed-order column sums over blocks of 256
+//          rows, then over the blocks in order (no atomics).
+// Each is one HBM pass over the rows; the norm costs ~0.2% of the LM head it
+// feeds, so it runs as its own launch ahead of the head instead of inside the
+// head's MFMA loop, which would repeat it once per vocabulary tile and add
+// VALU work to the loop that bounds the head.
+
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+
+namespace tim {
+namespace {
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ uint16_t to_bf16(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 1; off < 64; off *= 2) v = v + __shfl_xor(v, off);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_fwd(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
+                                                   int64_t T, int d, float eps, uint4* __restrict__ h,
+                                                   float* __restrict__ rstd) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int nc = d / 8;
+  const uint4* xr = x + t * nc;
+  float acc = 0.f;
+  for (int c = lane; c < nc; c += 64) {
+    const uint4 v = xr[c];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float a = bf16_lo(w[i]), b = bf16_hi(w[i]);
+      acc = __builtin_fmaf(a, a, acc);
+      acc = __builtin_fmaf(b, b, acc);
+    }
+  }
+  const float var = wave_sum(acc) / (float)d;
+  const float r = 1.0f / __builtin_sqrtf(var + eps);
+  if (rstd && lane == 0) rstd[t] = r;
+  uint4* hr = h + t * nc;
+  for (int c = lane; c < nc; c += 64) {
+    const uint4 v = xr[c];
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t g[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+    if (gamma) {
+      const uint4 gv = gamma[c];
+      g[0] = gv.x, g[1] = gv.y, g[2] = gv.z, g[3] = gv.w;
+    }
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float lo = bf16_lo((uint32_t)to_bf16(bf16_lo(w[i]) * r));
+      float hi = bf16_lo((uint32_t)to_bf16(bf16_hi(w[i]) * r));
+      if (gamma) {
+        lo = lo * bf16_lo(g[i]);
+        hi = hi * bf16_hi(g[i]);
+      }
+      o[i] = (uint32_t)to_bf16(lo) | ((uint32_t)to_bf16(hi) << 16);
+    }
+    hr[c] = uint4{o[0], o[1], o[2], o[3]};
+  }
+}
+
+__global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
+                                                     const float* __restrict__ rstd, const float4* __restrict__ G,
+                                                     int64_t T, int d, float4* __restrict__ dx) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;
+  const int nc = d / 8;
+  const uint4* xr = x + t * nc;
+  const float4* gr = G + t * (int64_t)(d / 4);
+  float acc = 0.f;
+  for (int c = lane; c < nc; c += 64) {
+    const uint4 v = xr[c];
+    const float4 g0 = gr[2 * c], g1 = gr[2 * c + 1];
+    const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t gm[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+    if (gamma) {
+      const uint4 gv = gamma[c];
+      gm[0] = gv.x, gm[1] = gv.y, gm[2] = gv.z, gm[3] = gv.w;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc = __builtin_fmaf(gg[2 * i] * bf16_lo(gm[i]), bf16_lo(w[i]), acc);
+      acc = __builtin_fmaf(gg[2 * i + 1] * bf16_hi(gm[i]), bf16_hi(w[i]), acc);
+    }
+  }
+  const float s = wave_sum(acc);
+  const float r = rstd[t];
+  const float c2 = ((r * r) * r) * s / (float)d;
+  float4* out = dx + t * (int64_t)(d / 4);
+  for (int c = lane; c < nc; c += 64) {
+    const uint4 v = xr[c];
+    const float4 g0 = gr[2 * c], g1 = gr[2 * c + 1];
+    const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t gm[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+    if (gamma) {
+      const uint4 gv = gamma[c];
+      gm[0] = gv.x, gm[1] = gv.y, gm[2] = gv.z, gm[3] = gv.w;
+    }
+    float o[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = r * (bf16_lo(gm[i]) * gg[2 * i]) - c2 * bf16_lo(w[i]);
+      o[2 * i + 1] = r * (bf16_hi(gm[i]) * gg[2 * i + 1]) - c2 * bf16_hi(w[i]);
+    }
+    out[2 * c] = float4{o[0], o[1], o[2], o[3]};
+    out[2 * c + 1] = float4{o[4], o[5], o[6], o[7]};
+  }
+}
+
+// Column sums of G x r over one block of up to 256 rows, rows in order.
+__global__ __launch_bounds__(256) void rmsnorm_dgamma_part(const uint16_t* __restrict__ x,
+                                                           const float* __restrict__ rstd,
+                                                           const float* __restrict__ G, int64_t T, int d,
+                                                           float* __restrict__ part) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= d) return;
+  const int64_t t0 = (int64_t)blockIdx.y * 256;
+  const int64_t t1 = (T - t0) < 256 ? T : t0 + 256;
+  float acc = 0.f;
+  for (int64_t t = t0; t < t1; ++t) {
+    const float xv = __uint_as_float((uint32_t)x[t * d + k] << 16);
+    acc = acc + (G[t * d + k] * xv) * rstd[t];
+  }
+  part[(int64_t)blockIdx.y * d + k] = acc;
+}
+
+// dg_k (+)= the blocks' sums in block order.
+__global__ __launch_bounds__(256) void rmsnorm_dgamma_final(const float* __restrict__ part, int n_blocks, int d,
+                                                            int accumulate, float* __restrict__ dg) {
+  const int k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= d) return;
+  float acc = accumulate ? dg[k] : 0.f;
+  for (int b = 0; b < n_blocks; ++b) acc = acc + part[(int64_t)b * d + k];
+  dg[k] = acc;
+}
+
+}  // namespace
+
+hipError_t launch_rmsnorm(const void* x, const void* gamma, int64_t T, int d, float eps, void* h, float* rstd,
+                          hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  const int64_t nb = (T + 3) / 4;
+  if (nb > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(rmsnorm_fwd, dim3((unsigned)nb), dim3(256), 0, s, (const uint4*)x, (const uint4*)gamma, T, d,
+                     eps, (uint4*)h, rstd);
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
+                                   int64_t T, int d, float* grad_x, float* grad_gamma, int accumulate, float* part,
+                                   hipStream_t s) {
+  if (T > 0 && grad_x) {
+    const int64_t nb = (T + 3) / 4;
+    if (nb > 0x7fffffff) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(rmsnorm_bwd_x, dim3((unsigned)nb), dim3(256), 0, s, (const uint4*)x, (const uint4*)gamma,
+                       rstd, (const float4*)grad_h, T, d, (float4*)grad_x);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (grad_gamma) {
+    const int64_t n_blocks = (T + 255) / 256;
+    if (n_blocks > 65535) return hipErrorInvalidValue;
+    const unsigned gx = (unsigned)((d + 255) / 256);
+    if (n_blocks > 0) {
+      hipLaunchKernelGGL(rmsnorm_dgamma_part, dim3(gx, (unsigned)n_blocks), dim3(256), 0, s, (const uint16_t*)x, rstd,
+                         grad_h, T, d, part);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(rmsnorm_dgamma_final, dim3(gx), dim3(256), 0, s, part, (int)n_blocks, d, accumulate,
+                       grad_gamma);
+    return hipGetLastError();
+  }
+  return hipSuccess;
+}
+
+}  // namespace tim

@@ -257,6 +257,29 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
   return TIM_OK;
 }
 
+tim_status tim_rmsnorm(const void* x, const void* gamma, int64_t T, int32_t d, float eps, void* h, float* rstd,
+                       hipStream_t stream) {
+  const tim_status st = tim::validate_rmsnorm(x, gamma, T, d, eps, h);
+  if (st != TIM_OK || T == 0) return st;
+  return hip_status(tim::launch_rmsnorm(x, gamma, T, d, eps, h, rstd, stream));
+}
+
+size_t tim_rmsnorm_backward_workspace_size(int64_t T, int32_t d) {
+  if (T <= 0 || tim::check_norm_shape(T, d) != TIM_OK) return 0;
+  return tim::rmsnorm_backward_workspace(T, d);
+}
+
+tim_status tim_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h, int64_t T,
+                                int32_t d, float* grad_x, float* grad_gamma, int32_t accumulate_grad_gamma,
+                                void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const tim_status st = tim::validate_rmsnorm_backward(x, gamma, rstd, grad_h, T, d, grad_x, grad_gamma,
+                                                       accumulate_grad_gamma, workspace, workspace_bytes);
+  if (st != TIM_OK || (!grad_x && !grad_gamma)) return st;
+  if (T == 0 && (!grad_gamma || accumulate_grad_gamma)) return TIM_OK;
+  return hip_status(tim::launch_rmsnorm_backward(x, gamma, rstd, grad_h, T, d, grad_x, grad_gamma,
+                                                 accumulate_grad_gamma, (float*)workspace, stream));
+}
+
 const char* tim_status_string(tim_status s) {
   switch (s) {
     case TIM_OK: return "TIM_OK";

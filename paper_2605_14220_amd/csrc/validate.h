@@ -174,4 +174,47 @@ inline tim_status validate_logit_grads(const void* hidden, const void* w, const 
   return TIM_OK;
 }
 
+// ------------------------------------------------------------ final RMS norm
+
+// Largest row count of the weight gradient (its column partial sums use one
+// grid row per 256 rows).
+constexpr int64_t kMaxNormRows = (int64_t)65535 * 256;
+
+inline tim_status check_norm_shape(int64_t T, int32_t d) {
+  if (T < 0 || T > kMaxNormRows) return TIM_ERR_SHAPE;
+  if (d <= 0 || d % 8 != 0) return TIM_ERR_SHAPE;
+  return TIM_OK;
+}
+
+inline size_t rmsnorm_backward_workspace(int64_t T, int32_t d) {
+  return (size_t)((T + 255) / 256) * (size_t)d * 4u;
+}
+
+inline tim_status validate_rmsnorm(const void* x, const void* gamma, int64_t T, int32_t d, float eps,
+                                   const void* h) {
+  const tim_status s = check_norm_shape(T, d);
+  if (s != TIM_OK) return s;
+  if (!std::isfinite(eps) || eps < 0.f) return TIM_ERR_VALUE;
+  if (T == 0) return TIM_OK;
+  if (!x || !h) return TIM_ERR_NULL;
+  if (!aligned16(x) || !aligned16(h) || (gamma && !aligned16(gamma))) return TIM_ERR_VALUE;
+  return TIM_OK;
+}
+
+inline tim_status validate_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
+                                            int64_t T, int32_t d, const float* grad_x, const float* grad_gamma,
+                                            int32_t accumulate, const void* ws, size_t ws_bytes) {
+  const tim_status s = check_norm_shape(T, d);
+  if (s != TIM_OK) return s;
+  if (accumulate != 0 && accumulate != 1) return TIM_ERR_VALUE;
+  if (!grad_x && !grad_gamma) return TIM_OK;
+  if (T > 0 && (!x || !rstd || !grad_h)) return TIM_ERR_NULL;
+  if ((x && !aligned16(x)) || (gamma && !aligned16(gamma)) || (grad_h && !aligned16(grad_h)) ||
+      (grad_x && !aligned16(grad_x)))
+    return TIM_ERR_VALUE;
+  if (grad_gamma && T > 0 && (!ws || !aligned16(ws) || ws_bytes < rmsnorm_backward_workspace(T, d)))
+    return TIM_ERR_WORKSPACE;
+  return TIM_OK;
+}
+
 }  // namespace tim

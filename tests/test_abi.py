@@ -39,7 +39,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == ["tim_logit_grads", "tim_logits", "tim_logprobs", "tim_logprobs_backward",
                      "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_partials",
-                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_status_string"]
+                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_rmsnorm",
+                     "tim_rmsnorm_backward", "tim_rmsnorm_backward_workspace_size", "tim_status_string"]
 
 
 def test_library_exports_every_declared_symbol(lib):
@@ -345,3 +346,62 @@ def _lg(lib, **kw):
 def test_logit_grads_rejects(lib, kw, expect):
     assert _lg(lib, **kw) == expect
     assert _lg(lib, T=0, out=None, hidden=None) == Status.OK
+
+
+# ---------------------------------------------------------------- final RMS norm
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(T=65535 * 256 + 1), Status.ERR_SHAPE),
+    (dict(d=0), Status.ERR_SHAPE),
+    (dict(d=12), Status.ERR_SHAPE),
+    (dict(eps=-1e-6), Status.ERR_VALUE),
+    (dict(eps=math.nan), Status.ERR_VALUE),
+    (dict(eps=math.inf), Status.ERR_VALUE),
+    (dict(x=None), Status.ERR_NULL),
+    (dict(h=None), Status.ERR_NULL),
+    (dict(x=FAKE_MIS), Status.ERR_VALUE),
+    (dict(h=FAKE_MIS), Status.ERR_VALUE),
+    (dict(gamma=FAKE_MIS), Status.ERR_VALUE),
+])
+def test_rmsnorm_rejects(lib, kw, expect):
+    g = lambda k, v: kw.get(k, v)
+    assert lib.tim_rmsnorm(g("x", FAKE), g("gamma", None), g("T", 8), g("d", 256), g("eps", 1e-6), g("h", FAKE),
+                           None, None) == expect
+
+
+def test_rmsnorm_T_zero_is_noop(lib):
+    assert lib.tim_rmsnorm(None, None, 0, 256, 1e-6, None, None, None) == Status.OK
+
+
+def _nb(lib, **kw):
+    g = lambda k, v: kw.get(k, v)
+    T, d = g("T", 8), g("d", 256)
+    return lib.tim_rmsnorm_backward(g("x", FAKE), g("gamma", None), g("rstd", FAKE), g("gh", FAKE), T, d,
+                                    g("gx", FAKE), g("gg", FAKE), g("acc", 0), g("ws", FAKE),
+                                    g("ws_bytes", ((T + 255) // 256) * d * 4), None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(d=4), Status.ERR_SHAPE),
+    (dict(acc=3), Status.ERR_VALUE),
+    (dict(x=None), Status.ERR_NULL),
+    (dict(rstd=None), Status.ERR_NULL),
+    (dict(gh=None), Status.ERR_NULL),
+    (dict(gh=FAKE_MIS), Status.ERR_VALUE),
+    (dict(gx=FAKE_MIS), Status.ERR_VALUE),
+    (dict(ws=None), Status.ERR_WORKSPACE),
+    (dict(ws_bytes=100), Status.ERR_WORKSPACE),
+])
+def test_rmsnorm_backward_rejects(lib, kw, expect):
+    assert _nb(lib, **kw) == expect
+
+
+def test_rmsnorm_backward_noops_and_workspace(lib):
+    assert _nb(lib, gx=None, gg=None, x=None, ws=None) == Status.OK
+    assert _nb(lib, gg=None, ws=None, gx=None) == Status.OK
+    assert _nb(lib, T=0, gx=None, acc=1, x=None, ws=None) == Status.OK
+    assert lib.tim_rmsnorm_backward_workspace_size(1000, 4096) == 4 * 4096 * 4
+    assert lib.tim_rmsnorm_backward_workspace_size(0, 4096) == 0
+    assert lib.tim_rmsnorm_backward_workspace_size(10, 12) == 0
