@@ -15,9 +15,12 @@ Parity status (each function's own docstring names its pins):
   forward, float64 autograd, closed forms, the zero-sum identity).
 * ``rmsnorm``, ``rmsnorm_grads``, ``round_bf16``  pinned (torch's bf16 cast and
   float64 rms_norm, ties, closed forms, finite differences, float64 autograd).
+* ``ppo_loss``  pinned (float64 autograd through the textbook loss, closed
+  forms, clip regions, response sums).
 """
 
 from .logprobs import bf16_to_f64, logits, logprobs  # noqa: F401
 from .grads import logit_grads, logprob_grads  # noqa: F401
 from .mismatch import mismatch, mismatch_seq  # noqa: F401
+from .ppo import ppo_loss  # noqa: F401
 from .rmsnorm import f64_to_bf16_bits, rmsnorm, rmsnorm_grads, round_bf16  # noqa: F401

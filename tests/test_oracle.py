@@ -653,3 +653,81 @@ def test_rmsnorm_grads_match_torch_autograd_and_scale_identity():
     a = oracle.rmsnorm_grads(xb, None, 1e-6, G)
     b = oracle.rmsnorm_grads(xb, _bits(np.ones(d)), 1e-6, G)
     np.testing.assert_array_equal(a[0], b[0])
+
+
+# ---------------------------------------------------------------- PPO / GRPO token loss
+
+def _ppo_case(seed, T=40, n_seq=5):
+    rng = np.random.default_rng(seed)
+    lens = rng.multinomial(T - n_seq, np.ones(n_seq) / n_seq) + 1
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    lo = -rng.exponential(2.0, T)
+    lp = lo + rng.normal(0, 0.3, T)
+    A = rng.normal(0, 1, T)
+    w = rng.uniform(0, 2, T)
+    return lp, lo, A, w, cu
+
+
+@pytest.mark.parametrize("eps_low,eps_high", [(0.2, 0.2), (0.2, 0.28)])
+def test_ppo_matches_torch_autograd(eps_low, eps_high):
+    lp, lo, A, w, cu = _ppo_case(31)
+    n = len(cu) - 1
+    out = oracle.ppo_loss(lp, lo, A, cu, eps_low, eps_high, w)
+    x = torch.tensor(lp, requires_grad=True)
+    r = torch.exp(x - torch.tensor(lo))
+    At = torch.tensor(A)
+    tok = -torch.minimum(r * At, torch.clamp(r, 1 - eps_low, 1 + eps_high) * At) * torch.tensor(w)
+    seq = torch.stack([tok[cu[j]:cu[j + 1]].sum() for j in range(n)])
+    L = seq.mean()
+    L.backward()
+    np.testing.assert_allclose(out["token_loss"], tok.detach().numpy(), rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(out["seq_loss"], seq.detach().numpy(), rtol=1e-13, atol=1e-14)
+    assert abs(out["batch_loss"] - L.item()) <= 1e-13
+    np.testing.assert_allclose(out["grad"], x.grad.numpy(), rtol=1e-13, atol=1e-15)
+    # C has the gradient of -r A and vanishes at r = 1
+    x2 = torch.tensor(lp, requires_grad=True)
+    r2 = torch.exp(x2 - torch.tensor(lo))
+    (-(r2 - 1) * At).sum().backward()
+    np.testing.assert_allclose(x2.grad.numpy(), (-At * r2).detach().numpy(), rtol=1e-14)
+    np.testing.assert_allclose(out["contribution"], (-(r2 - 1) * At).detach().numpy(), rtol=1e-14, atol=1e-15)
+
+
+def test_ppo_closed_forms_and_clip_regions():
+    lp, lo, A, w, cu = _ppo_case(32)
+    n = len(cu) - 1
+    same = oracle.ppo_loss(lo, lo, A, cu, 0.2, 0.3, w)      # r = 1
+    np.testing.assert_array_equal(same["token_loss"], -A * w)
+    np.testing.assert_allclose(same["grad"], -A * w / n, rtol=1e-15)
+    np.testing.assert_array_equal(same["contribution"], 0.0)
+    assert not same["clipped"].any()
+    zero = oracle.ppo_loss(lp, lo, np.zeros_like(A), cu, 0.2, 0.3, w)
+    assert not zero["token_loss"].any() and not zero["grad"].any() and zero["batch_loss"] == 0.0
+    # one token per case: (delta, A) -> (loss, grad factor, clipped)
+    el, eh = 0.2, 0.3
+    cases = [(math.log(1.5), 2.0, -2.0 * (1 + eh), 0.0, True),      # A > 0, above 1 + eps_high: clipped
+             (math.log(0.5), 2.0, -2.0 * 0.5, -2.0 * 0.5, False),   # A > 0, below 1 - eps_low: unclipped
+             (math.log(0.5), -2.0, 2.0 * (1 - el), 0.0, True),      # A < 0, below 1 - eps_low: clipped
+             (math.log(1.5), -2.0, 2.0 * 1.5, 2.0 * 1.5, False),    # A < 0, above 1 + eps_high: unclipped
+             (math.log(1.1), 2.0, -2.0 * 1.1, -2.0 * 1.1, False)]   # inside: unclipped
+    for dlt, a, loss, grad, clipped in cases:
+        o = oracle.ppo_loss(np.array([dlt - 1.0]), np.array([-1.0]), np.array([a]), [0, 1], el, eh)
+        assert abs(o["token_loss"][0] - loss) <= 1e-12, (dlt, a, o["token_loss"][0], loss)
+        assert abs(o["grad"][0] - grad) <= 1e-12, (dlt, a, o["grad"][0], grad)
+        assert bool(o["clipped"][0]) == clipped
+        assert o["batch_loss"] == o["seq_loss"][0] == o["token_loss"][0]
+
+
+def test_ppo_batch_is_mean_of_response_sums_and_order_free():
+    lp, lo, A, w, cu = _ppo_case(33, T=60, n_seq=6)
+    out = oracle.ppo_loss(lp, lo, A, cu, 0.2, 0.2, w)
+    assert abs(out["batch_loss"] - out["seq_loss"].mean()) <= 1e-14
+    for j in range(len(cu) - 1):
+        assert abs(out["seq_loss"][j] - out["token_loss"][cu[j]:cu[j + 1]].sum()) <= 1e-13
+    # responses in another order: the same response sums, permuted
+    order = [3, 0, 5, 1, 4, 2]
+    segs = [(cu[j], cu[j + 1]) for j in order]
+    idx = np.concatenate([np.arange(a, b) for a, b in segs])
+    cu2 = np.concatenate([[0], np.cumsum([b - a for a, b in segs])])
+    out2 = oracle.ppo_loss(lp[idx], lo[idx], A[idx], cu2, 0.2, 0.2, w[idx])
+    np.testing.assert_array_equal(out2["seq_loss"], out["seq_loss"][order])
+    assert abs(out2["batch_loss"] - out["batch_loss"]) <= 1e-15

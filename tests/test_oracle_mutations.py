@@ -50,6 +50,15 @@ MUTATIONS = [
     ("rmsnorm.py", "(r ** 3 * s / d)", "(r ** 2 * s / d)"),
     ("rmsnorm.py", "s = (G * g[None, :] * x)", "s = (G * x)"),
     ("rmsnorm.py", "dg = (G * x * r[:, None])", "dg = (G * x)"),
+    ("ppo.py", "r = np.exp(lp - lo)", "r = np.exp(lo - lp)"),
+    ("ppo.py", "L = -np.minimum(unclipped, clipped_term)", "L = -np.maximum(unclipped, clipped_term)"),
+    ("ppo.py", "np.clip(r, 1.0 - eps_low, 1.0 + eps_high)", "np.clip(r, 1.0 - eps_high, 1.0 + eps_low)"),
+    ("ppo.py", "np.where(use_unclipped, -A * r, 0.0)", "np.where(use_unclipped, -A, 0.0)"),
+    ("ppo.py", "grad_tok[s0:s1] / n", "grad_tok[s0:s1]"),
+    ("ppo.py", "C = -(r - 1.0) * A", "C = (r - 1.0) * A"),
+    ("ppo.py", "token_loss[s0:s1] = w[s0:s1] * L[s0:s1]", "token_loss[s0:s1] = L[s0:s1]"),
+    ("ppo.py", "math.fsum(seq.tolist()) / n", "math.fsum(seq.tolist()) / T"),
+    ("ppo.py", "use_unclipped = unclipped <= clipped_term", "use_unclipped = unclipped >= clipped_term"),
 ]
 
 
