@@ -261,6 +261,24 @@ def main(argv=None):
            "max_k3_score": float(seq_out[0].max().item())}
     log(f"[bench] sequence-level K3 scores / mask / weights over {len(lens)} responses: {seq_ms * 1e3:.1f} us/call")
 
+    # clipped PPO/GRPO loss over the stream (logp_b stands in for the old log-probs), weighted by the
+    # sequence-level TIS + RS weights, with its gradient
+    adv = torch.repeat_interleave(torch.randn(len(lens), generator=torch.Generator(device="cpu").manual_seed(96)),
+                                  torch.as_tensor(lens)).float().to(dev)
+    pl = tim.ppo_loss(logp, logp_b, adv, cu, 0.2, 0.28, seq_out[2])
+    for _ in range(3):
+        tim.ppo_loss(logp, logp_b, adv, cu, 0.2, 0.28, seq_out[2], out=pl)
+    q0.record(stream)
+    for _ in range(n_seq_calls):
+        tim.ppo_loss(logp, logp_b, adv, cu, 0.2, 0.28, seq_out[2], out=pl)
+    q1.record(stream)
+    torch.cuda.synchronize()
+    ppo_ms = q0.elapsed_time(q1) / n_seq_calls
+    ppo = {"responses": len(lens), "tokens": T, "ms_per_call": ppo_ms, "tokens_per_s": T / (ppo_ms / 1e3),
+           "bytes_per_call": 16.0 * T + 13.0 * T + 24.0 * len(lens),
+           "batch_loss": float(pl["batch_loss"].item()), "clipped_tokens": int(pl["clipped"].sum().item())}
+    log(f"[bench] PPO/GRPO loss + gradient over {len(lens)} responses: {ppo_ms * 1e3:.1f} us/call")
+
     # the final RMS norm in front of the head over the whole stream (HBM-bound), and its backward
     gam = (1.0 + 0.1 * torch.randn(d, generator=torch.Generator(device="cpu").manual_seed(98))).to(torch.bfloat16).to(dev)
     h_n = torch.empty_like(h)
@@ -381,6 +399,7 @@ def main(argv=None):
         "sequence_mismatch": seq,
         "backward": bwd,
         "rmsnorm": norm,
+        "ppo_loss": ppo,
     }
     print(json.dumps(out), flush=True)
 

@@ -246,6 +246,37 @@ tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_
                            const float* grad_logp, const float* grad_entropy,
                            void* dlogits, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Clipped PPO / GRPO token loss over a packed stream of n_seq responses
+ * (Section 4.1: Eq. 2's surrogate on Eq. 3's ratio, Eq. 5's zero-centred
+ * contribution; Section 4.2's token weights), summed over each response and
+ * averaged over the responses:
+ *   r_t          = exp(logp[t] - logp_old[t])    (logp_old: the trainer's recomputed
+ *                                                 or the rollout's old log-probs)
+ *   L_t          = -min(r_t A_t, clip(r_t, 1 - eps_low, 1 + eps_high) A_t)
+ *   token_loss[t]= w_t L_t                        (w = weight[t], or 1 when NULL)
+ *   seq_loss[j]  = sum over response j of token_loss      (fp64, fixed order)
+ *   batch_loss[0]= (1 / n_seq) sum_j seq_loss[j]          (fp64)
+ *   grad_logp[t] = d batch_loss / d logp[t] = w_t (-A_t r_t) / n_seq where the
+ *                  unclipped term is the minimum, else 0 (feeds tim_logprobs_backward)
+ *   contribution[t] = -(r_t - 1) A_t               (C(r), the same gradient as -r A)
+ *   clipped[t]   = 1 where the clipped term is strictly the minimum (zero gradient)
+ * delta = logp - logp_old is formed exactly in fp64, r and the losses in fp64
+ * (token outputs rounded once to fp32); the clip decision is taken on delta
+ * against log1p(eps_high) / log1p(-eps_low), which is exact. Responses are
+ * given by cu_seqlens (int64 [n_seq + 1], DEVICE, clamped into [0, T] as in
+ * tim_mismatch_seq); tokens outside every response are not written. A
+ * response's outputs are bitwise the same wherever it sits in the stream.
+ * advantages fp32 [T] (GRPO: the response's advantage on each of its tokens).
+ * All outputs are device pointers and may be NULL, except that batch_loss needs
+ * seq_loss. eps_low in [0, 1), eps_high >= 0 (the paper's single eps is both).
+ * n_seq == 0 is a no-op. Errors: TIM_ERR_SHAPE for T < 0 or a bad n_seq;
+ * TIM_ERR_VALUE for bad eps; TIM_ERR_NULL for NULL cu_seqlens, NULL inputs with
+ * T > 0, or batch_loss without seq_loss. */
+tim_status tim_ppo_loss(const float* logp, const float* logp_old, const float* advantages, const float* weight,
+                        int64_t T, const int64_t* cu_seqlens, int64_t n_seq, float eps_low, float eps_high,
+                        double* seq_loss, double* batch_loss, float* token_loss, float* grad_logp,
+                        float* contribution, uint8_t* clipped, hipStream_t stream);
+
 /* Final RMS normalisation in front of the LM head (Section 3.1 lists RMSNorm
  * among the batch-invariant kernels; root-mean-square layer normalisation).
  * Row t of x (bf16 [T, d] row-major, 16-byte aligned, d a multiple of 8):

@@ -101,6 +101,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tim_rmsnorm_backward.restype = c.c_int
     lib.tim_rmsnorm_backward.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32,
                                          c.c_void_p, c.c_void_p, c.c_int32, c.c_void_p, c.c_size_t, c.c_void_p]
+    lib.tim_ppo_loss.restype = c.c_int
+    lib.tim_ppo_loss.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_void_p, c.c_int64,
+                                 c.c_float, c.c_float, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p, c.c_void_p,
+                                 c.c_void_p, c.c_void_p]
     lib.tim_logits.restype = c.c_int
     lib.tim_logits.argtypes = [c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32, c.c_float,
                                c.c_int32, c.c_void_p, c.c_void_p]
@@ -381,3 +385,34 @@ def logprobs_from_residual(x: torch.Tensor, gamma: torch.Tensor | None, w_vocab:
     h, rstd = rmsnorm(x, gamma, eps)
     lp, ent, lse = logprobs(h, w_vocab, tokens, temperature, **kw)
     return lp, ent, lse, h, rstd
+
+
+def ppo_loss(logp: torch.Tensor, logp_old: torch.Tensor, advantages: torch.Tensor, cu_seqlens: torch.Tensor,
+             eps_low: float = 0.2, eps_high: float = 0.2, weight: torch.Tensor | None = None,
+             out: dict | None = None) -> dict:
+    """Clipped PPO/GRPO loss of a packed stream (see include/tim.h): dict with seq_loss fp64 [n],
+    batch_loss fp64 [1], token_loss / grad / contribution fp32 [T] and clipped uint8 [T]
+    (freshly allocated outputs are zero outside every response; `out` reuses a previous dict)."""
+    lib = load_library()
+    for t in (logp, logp_old, advantages, weight):
+        if t is not None and (t.dtype != torch.float32 or t.shape != logp.shape):
+            raise TypeError("tim.ppo_loss: per-token inputs must be fp32 of one shape")
+    if cu_seqlens.dtype != torch.int64 or cu_seqlens.dim() != 1 or cu_seqlens.numel() < 1:
+        raise TypeError("tim.ppo_loss: cu_seqlens must be a non-empty int64 vector")
+    _require_gpu(logp, logp_old, advantages, weight, cu_seqlens)
+    T = logp.numel()
+    n = cu_seqlens.numel() - 1
+    dev = logp.device
+    if out is not None:
+        _require_gpu(*out.values())
+    out = out or {"seq_loss": torch.zeros(n, dtype=torch.float64, device=dev),
+           "batch_loss": torch.zeros(1, dtype=torch.float64, device=dev),
+           "token_loss": torch.zeros(T, dtype=torch.float32, device=dev),
+           "grad": torch.zeros(T, dtype=torch.float32, device=dev),
+           "contribution": torch.zeros(T, dtype=torch.float32, device=dev),
+           "clipped": torch.zeros(T, dtype=torch.uint8, device=dev)}
+    _check(lib.tim_ppo_loss(_ptr(logp), _ptr(logp_old), _ptr(advantages), _ptr(weight), T, _ptr(cu_seqlens), n,
+                            float(eps_low), float(eps_high), _ptr(out["seq_loss"]), _ptr(out["batch_loss"]),
+                            _ptr(out["token_loss"]), _ptr(out["grad"]), _ptr(out["contribution"]),
+                            _ptr(out["clipped"]), _stream(dev)))
+    return out

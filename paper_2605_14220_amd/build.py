@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libtim.so")
-SOURCES = ["lmhead.hip", "lmgrad.hip", "rmsnorm.hip", "mismatch.hip", "seqstats.hip", "tim_api.hip"]
+SOURCES = ["lmhead.hip", "lmgrad.hip", "rmsnorm.hip", "mismatch.hip", "seqstats.hip", "ppo.hip", "tim_api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -91,6 +91,18 @@ hipError_t launch_rmsnorm(const void* x, const void* gamma, int64_t T, int d, fl
 hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
                                    int64_t T, int d, float* grad_x, float* grad_gamma, int accumulate, float* part,
                                    hipStream_t s);
+// Clipped PPO/GRPO loss constants, formed on the host in fp64.
+struct PpoParams {
+  double lo_threshold;  // log1p(-eps_low): A < 0 clips below it
+  double hi_threshold;  // log1p(eps_high): A > 0 clips above it
+  double clip_lo;       // 1 - eps_low
+  double clip_hi;       // 1 + eps_high
+  double inv_n;         // 1 / number of responses (the batch mean)
+};
+hipError_t launch_ppo_loss(const float* logp, const float* logp_old, const float* advantages, const float* weight,
+                           int64_t T, const int64_t* cu_seqlens, int64_t n_seq, const PpoParams& p, double* seq_loss,
+                           double* batch_loss, float* token_loss, float* grad, float* contrib, uint8_t* clipped,
+                           hipStream_t s);
 hipError_t launch_mismatch(const float* a, const float* b, int64_t n, float C,
                            float* log_ratio, float* k3, float* w, hipStream_t s);
 // Per-response score / keep and per-token weights of a packed stream (one

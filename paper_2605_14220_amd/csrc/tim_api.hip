@@ -7,6 +7,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include "kernels.h"
 #include "tim.h"
 #include "validate.h"
@@ -278,6 +280,24 @@ tim_status tim_rmsnorm_backward(const void* x, const void* gamma, const float* r
   if (T == 0 && (!grad_gamma || accumulate_grad_gamma)) return TIM_OK;
   return hip_status(tim::launch_rmsnorm_backward(x, gamma, rstd, grad_h, T, d, grad_x, grad_gamma,
                                                  accumulate_grad_gamma, (float*)workspace, stream));
+}
+
+tim_status tim_ppo_loss(const float* logp, const float* logp_old, const float* advantages, const float* weight,
+                        int64_t T, const int64_t* cu_seqlens, int64_t n_seq, float eps_low, float eps_high,
+                        double* seq_loss, double* batch_loss, float* token_loss, float* grad_logp,
+                        float* contribution, uint8_t* clipped, hipStream_t stream) {
+  const tim_status st = tim::validate_ppo(logp, logp_old, advantages, T, cu_seqlens, n_seq, eps_low, eps_high,
+                                          seq_loss, batch_loss);
+  if (st != TIM_OK || n_seq == 0) return st;
+  if (!seq_loss && !batch_loss && !token_loss && !grad_logp && !contribution && !clipped) return TIM_OK;
+  tim::PpoParams p;
+  p.lo_threshold = std::log1p(-(double)eps_low);
+  p.hi_threshold = std::log1p((double)eps_high);
+  p.clip_lo = 1.0 - (double)eps_low;
+  p.clip_hi = 1.0 + (double)eps_high;
+  p.inv_n = 1.0 / (double)n_seq;
+  return hip_status(tim::launch_ppo_loss(logp, logp_old, advantages, weight, T, cu_seqlens, n_seq, p, seq_loss,
+                                         batch_loss, token_loss, grad_logp, contribution, clipped, stream));
 }
 
 const char* tim_status_string(tim_status s) {

@@ -174,6 +174,21 @@ inline tim_status validate_logit_grads(const void* hidden, const void* w, const 
   return TIM_OK;
 }
 
+// ------------------------------------------------------------ PPO / GRPO loss
+
+inline tim_status validate_ppo(const float* logp, const float* logp_old, const float* adv, int64_t T,
+                               const int64_t* cu, int64_t n_seq, float eps_low, float eps_high,
+                               const double* seq_loss, const double* batch_loss) {
+  if (T < 0 || n_seq < 0 || n_seq > INT32_MAX) return TIM_ERR_SHAPE;
+  if (!std::isfinite(eps_low) || !std::isfinite(eps_high) || eps_low < 0.f || eps_low >= 1.f || eps_high < 0.f)
+    return TIM_ERR_VALUE;
+  if (n_seq == 0) return TIM_OK;
+  if (!cu) return TIM_ERR_NULL;
+  if (T > 0 && (!logp || !logp_old || !adv)) return TIM_ERR_NULL;
+  if (batch_loss && !seq_loss) return TIM_ERR_NULL;
+  return TIM_OK;
+}
+
 // ------------------------------------------------------------ final RMS norm
 
 // Largest row count of the weight gradient (its column partial sums use one

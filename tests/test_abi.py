@@ -39,7 +39,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == ["tim_logit_grads", "tim_logits", "tim_logprobs", "tim_logprobs_backward",
                      "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_partials",
-                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_rmsnorm",
+                     "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_ppo_loss", "tim_rmsnorm",
                      "tim_rmsnorm_backward", "tim_rmsnorm_backward_workspace_size", "tim_status_string"]
 
 
@@ -405,3 +405,34 @@ def test_rmsnorm_backward_noops_and_workspace(lib):
     assert lib.tim_rmsnorm_backward_workspace_size(1000, 4096) == 4 * 4096 * 4
     assert lib.tim_rmsnorm_backward_workspace_size(0, 4096) == 0
     assert lib.tim_rmsnorm_backward_workspace_size(10, 12) == 0
+
+
+# ---------------------------------------------------------------- PPO / GRPO loss
+
+def _ppo(lib, **kw):
+    g = lambda k, v: kw.get(k, v)
+    return lib.tim_ppo_loss(g("lp", FAKE), g("lo", FAKE), g("adv", FAKE), None, g("T", 8), g("cu", FAKE), g("n", 2),
+                            g("el", 0.2), g("eh", 0.2), g("seq", FAKE), g("batch", None), None, None, None, None, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(n=-1), Status.ERR_SHAPE),
+    (dict(n=2 ** 31), Status.ERR_SHAPE),
+    (dict(el=-0.1), Status.ERR_VALUE),
+    (dict(el=1.0), Status.ERR_VALUE),
+    (dict(eh=-0.1), Status.ERR_VALUE),
+    (dict(eh=math.nan), Status.ERR_VALUE),
+    (dict(cu=None), Status.ERR_NULL),
+    (dict(lp=None), Status.ERR_NULL),
+    (dict(lo=None), Status.ERR_NULL),
+    (dict(adv=None), Status.ERR_NULL),
+    (dict(seq=None, batch=FAKE), Status.ERR_NULL),
+])
+def test_ppo_rejects(lib, kw, expect):
+    assert _ppo(lib, **kw) == expect
+
+
+def test_ppo_noops(lib):
+    assert _ppo(lib, n=0, cu=None, lp=None) == Status.OK
+    assert _ppo(lib, seq=None) == Status.OK          # no outputs requested
