@@ -46,6 +46,7 @@ struct EpiDlogits {
   using Args = DlogitsArgs;
   static constexpr bool kTokens = true;
   static constexpr bool kCoef = true;
+  static constexpr int kGroupA = TIM_GROUP_V;
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
   __device__ static TileOps ops(const Args& a) {
@@ -105,6 +106,7 @@ struct EpiStore {
   using Args = GemmArgs;
   static constexpr bool kTokens = false;
   static constexpr bool kCoef = false;
+  static constexpr int kGroupA = TIM_STORE_GROUP;
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
   __device__ static TileOps ops(const Args& a) {

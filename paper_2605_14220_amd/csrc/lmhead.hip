@@ -200,6 +200,7 @@ struct EpiPartials {
   using Args = LmHeadArgs;
   static constexpr bool kTokens = !DUMP;
   static constexpr bool kCoef = false;
+  static constexpr int kGroupA = TIM_GROUP_V;
   template <int BT>
   static constexpr int scratch_bytes() { return 7 * BT * 4; }
   __device__ static TileOps ops(const Args& a) {

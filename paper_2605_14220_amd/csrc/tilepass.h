@@ -45,6 +45,9 @@ struct rsrc_t {
 #ifndef TIM_GROUP_V
 #define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
 #endif
+#ifndef TIM_STORE_GROUP
+#define TIM_STORE_GROUP 8  // A tiles per group in the tile order of the plain products
+#endif
 #ifndef TIM_LOAD_AUX
 #define TIM_LOAD_AUX 0     // cache-policy bits of the global->LDS loads (gfx950 sc0=1, nt=2, sc1=16)
 #endif
@@ -156,13 +159,12 @@ __device__ __forceinline__ void stage_barrier() {
 // which does not fill the pipe -- shrinks.
 __device__ __forceinline__ void region_a_prio() { __builtin_amdgcn_s_setprio(0); }
 
-// Tile order: logical id -> (vocab tile, row tile), walking groups of
-// TIM_GROUP_V vocab tiles with the row tiles outer and the vocab tiles inner,
-// so that the workgroups resident on one XCD at a time (consecutive logical
-// ids, see lmhead_partials) share W tiles and hidden-state tiles through that
-// XCD's L2.
+// Tile order: logical id -> (A tile, B tile), walking groups of GV A tiles
+// with the B tiles outer and the A tiles inner, so that the workgroups
+// resident on one XCD at a time (consecutive logical ids, see tile_pass) share
+// A tiles and B tiles through that XCD's L2.
+template <int GV>
 __device__ __forceinline__ void tile_of_lid(int lid, int n_vt, int n_tt, int& vt, int& tt) {
-  constexpr int GV = TIM_GROUP_V;
   const int group = lid / (GV * n_tt);
   const int first = group * GV;
   const int gv = (n_vt - first) < GV ? (n_vt - first) : GV;
@@ -352,7 +354,7 @@ struct TileCtx {
   rsrc_t wr, hr, tr, cr;
 };
 
-template <int NTB, int WT>
+template <int NTB, int WT, int GV>
 __device__ __forceinline__ TileCtx<NTB, WT> make_tile(const TileOps& o, int lid, int n_vt, int n_tt, int wave,
                                                       int lane) {
   constexpr int BT = Tile<NTB, WT>::BT;
@@ -362,7 +364,7 @@ __device__ __forceinline__ TileCtx<NTB, WT> make_tile(const TileOps& o, int lid,
   asm volatile("" : "+v"(lane));
   TileCtx<NTB, WT> c;
   int tt;
-  tile_of_lid(lid, n_vt, n_tt, c.vt, tt);
+  tile_of_lid<GV>(lid, n_vt, n_tt, c.vt, tt);
   c.v0 = (int64_t)c.vt * kVocabTile;
   c.t0 = (int64_t)tt * BT;
   const int w_rows = (o.a_rows - c.v0) < kVocabTile ? (int)(o.a_rows - c.v0) : kVocabTile;
@@ -443,7 +445,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   const int nk_q = nk / 4;     // stages per quarter (SPLITK4)
   constexpr int kStep = kKS * 2;
 
-  TC cur = make_tile<NTB, WT>(ops, start + j, n_vt, n_tt, wave, lane0);
+  TC cur = make_tile<NTB, WT, E::kGroupA>(ops, start + j, n_vt, n_tt, wave, lane0);
 
   // prologue: the tile's row data and stages 0 .. kNBuf - 1
   auto prologue = [&]() {
@@ -503,7 +505,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     // through the epilogue), to this tile's own stages again. Stage k sits in
     // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
     {
-      const TC nx = make_tile<NTB, WT>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
+      const TC nx = make_tile<NTB, WT, E::kGroupA>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
 #pragma unroll
       for (int t = 0; t < kNBuf; ++t) {
         k = nk - kNBuf + t;
@@ -544,7 +546,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     par ^= 1;
     if (!has_next) break;
     j += w_x;
-    cur = make_tile<NTB, WT>(ops, next_lid, n_vt, n_tt, wave, lane);
+    cur = make_tile<NTB, WT, E::kGroupA>(ops, next_lid, n_vt, n_tt, wave, lane);
     if constexpr (!kSep) {
       __syncthreads();  // the epilogue's reads of the first buffer are done
       prologue();
