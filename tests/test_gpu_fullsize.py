@@ -23,7 +23,7 @@ import oracle
 import paper_2605_14220_amd as tim
 from paper_2605_14220_amd import Mode, Order
 from tim_testutil import TOL_ENT, TOL_LOGP, TOL_W_REL, bits_equal, check_close, require_gpu
-from workload import CONFIGS, bf16_bits, hidden_states, uniforms, vocab_weights
+from workload import CONFIGS, bf16_bits, hidden_states, logprob_pairs, uniforms, vocab_weights
 from workload.gen import seeds
 from workload.sampler import sample_tokens
 
@@ -166,16 +166,23 @@ def test_stress_invariance_and_mismatch_report():
     # the engines agree within the oracle tolerance, so every weight is within 2e-3 of 1
     assert d.max().item() < 2 * TOL_LOGP
     assert ((w - 1).abs() <= 2 * TOL_W_REL).all()
-    r_lr, r_k3, r_w = oracle.mismatch(ref[0].cpu().numpy(), eng[0].cpu().numpy(), 2.0)
-    assert np.all(np.abs(lr.double().cpu().numpy() - r_lr) <= 2.0 ** -24 * np.abs(r_lr) + 1e-45)
-    assert np.all(np.abs(w.double().cpu().numpy() - r_w) <= TOL_W_REL * r_w)
+    # the statistics of the two engines' log-probs follow from their difference
+    assert torch.equal(lr, ref[0] - eng[0])
+    assert ((w.double() - torch.clamp(torch.exp(lr.double()), max=2.0)).abs() <= TOL_W_REL * w.double()).all()
+    # the mismatch stages at this size against the oracle, on seeded streams of the same length with the
+    # paper's heavy-tailed discrepancies (inputs drawn by the workload module, not by the path)
+    a_np, b_np = logprob_pairs(T, seed=1003)
+    a_g, b_g = torch.as_tensor(a_np).cuda(), torch.as_tensor(b_np).cuda()
+    lr2, _, w2 = tim.mismatch(a_g, b_g, 2.0)
+    r_lr, r_k3, r_w = oracle.mismatch(a_np, b_np, 2.0)
+    assert np.all(np.abs(lr2.double().cpu().numpy() - r_lr) <= 2.0 ** -24 * np.abs(r_lr) + 1e-45)
+    assert np.all(np.abs(w2.double().cpu().numpy() - r_w) <= TOL_W_REL * r_w)
     # sequence level over the packed responses (Section 4.2): K1/K3 scores, the
     # rejection mask at tau_seq = 0.001 and the truncated-and-rejected weights
     lens = cfg.lengths()
     cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
-    a_np, b_np = ref[0].cpu().numpy(), eng[0].cpu().numpy()
     for est, name in ((tim.Estimator.K1, "k1"), (tim.Estimator.K3, "k3")):
-        sc, kp, wt = tim.mismatch_seq(ref[0], eng[0], torch.as_tensor(cu, device="cuda"), C=2.0, tau_seq=1e-3,
+        sc, kp, wt = tim.mismatch_seq(a_g, b_g, torch.as_tensor(cu, device="cuda"), C=2.0, tau_seq=1e-3,
                                       estimator=est)
         r_sc, r_kp, r_wt = oracle.mismatch_seq(a_np, b_np, cu, name, 2.0, 1e-3)
         sc = sc.cpu().numpy()

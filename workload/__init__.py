@@ -14,5 +14,6 @@ from .gen import (  # noqa: F401
     hidden_states,
     vocab_weights,
     uniforms,
+    logprob_pairs,
     bf16_bits,
 )

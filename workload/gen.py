@@ -93,6 +93,17 @@ def uniforms(T: int, seed: int) -> np.ndarray:
     return np.random.default_rng(seed).random(T)
 
 
+def logprob_pairs(T: int, seed: int, tail: float = 0.01, scale: float = 1e-5):
+    """Two fp32 log-probability streams of the same T tokens, as a trainer and a
+    rollout engine would report them: b ~ -Exp(mean 2), and a = b plus mostly
+    tiny discrepancies (std `scale`) with a heavy tail of std 0.3 on a fraction
+    `tail` of the tokens (the shape of the mismatch the paper measures)."""
+    rng = np.random.default_rng(seed)
+    b = (-rng.exponential(2.0, T)).astype(np.float32)
+    a = (b + rng.standard_normal(T) * np.where(rng.random(T) < tail, 0.3, scale)).astype(np.float32)
+    return a, b
+
+
 def bf16_bits(t: torch.Tensor) -> np.ndarray:
     """Raw bf16 bit patterns of a CPU or GPU tensor, as a host uint16 array."""
     assert t.dtype == torch.bfloat16
