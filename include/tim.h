@@ -70,7 +70,9 @@ typedef enum {
 /* Bytes of device workspace tim_logprobs needs for these arguments:
  * rows_per_launch * ceil(V / TIM_VOCAB_TILE) * 16, where rows_per_launch is T
  * in rollout mode and min(T, micro_batch) in training mode (micro_batch 0 means
- * T). Returns 0 for invalid arguments or T == 0. Pure host function. */
+ * T); in rollout mode with T <= 64 (a decode batch, whose partials may be
+ * taken over half tiles) T * ceil(V / (TIM_VOCAB_TILE / 2)) * 16. Returns 0 for
+ * invalid arguments or T == 0. Pure host function. */
 size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch);
 
 /* Token log-probabilities and entropies of T rows (Section 2, Eq. 1's terms).
@@ -95,10 +97,13 @@ size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode
  *
  * Arithmetic: bf16 x bf16 products accumulated in fp32 by MFMA with the
  * hidden dimension in ascending order; fp32 softmax partials per tile of
- * TIM_VOCAB_TILE vocabulary entries; partials merged by a fixed balanced tree
- * over the tile index. None of this depends on T, mode, micro_batch or a row's
- * position in the batch, so with TIM_ORDER_INVARIANT a row's outputs are
- * bitwise identical however it is batched. NaN or Inf in the inputs
+ * TIM_VOCAB_TILE vocabulary entries, each the merge of its two halves' (lower
+ * half first); partials merged by a fixed balanced tree over the tile index.
+ * None of this depends on T, mode, micro_batch or a row's position in the
+ * batch (a decode batch of at most 64 rows may write the halves' partials
+ * and merge each pair in the merge pass, which gives the same bits), so with
+ * TIM_ORDER_INVARIANT a row's outputs are bitwise identical however it is
+ * batched. NaN or Inf in the inputs
  * propagates to that row's outputs. */
 tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens,
                         int64_t T, int32_t d, int32_t V, float temperature,
@@ -109,7 +114,8 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
 /* The two stages of tim_logprobs, for callers that schedule them themselves
  * (a profiler timing one kernel, or a vocabulary-sharded deployment that
  * exchanges partials between the stages). tim_logprobs over one launch's rows
- * is exactly tim_logprobs_partials followed by tim_logprobs_merge.
+ * gives exactly the outputs of tim_logprobs_partials followed by
+ * tim_logprobs_merge (whose partials are always per whole tile).
  *
  * tim_logprobs_partials: one launch over all T rows (no micro-batching; mode
  * only picks the row tile). Writes T * ceil(V / TIM_VOCAB_TILE) partials of

@@ -47,6 +47,7 @@ struct EpiDlogits {
   static constexpr bool kTokens = true;
   static constexpr bool kCoef = true;
   static constexpr int kGroupA = TIM_GROUP_V;
+  static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
   __device__ static TileOps ops(const Args& a) {
@@ -107,6 +108,7 @@ struct EpiStore {
   static constexpr bool kTokens = false;
   static constexpr bool kCoef = false;
   static constexpr int kGroupA = TIM_STORE_GROUP;
+  static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
   __device__ static TileOps ops(const Args& a) {

@@ -68,26 +68,31 @@ static_assert(kSteps == 2, "the operand double buffer alternates once per k-step
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
 
-// Workgroup shape: 2 waves along the vocab tile (128 entries, 8 blocks of 16,
-// each) times WT waves along the rows, each wave holding NTB * 32 rows (2 * NTB
-// blocks of 16).
-template <int NTB, int WT>
+// Workgroup shape: NV waves along the A tile (128 entries, 8 blocks of 16,
+// each; NV = 2 covers a vocabulary tile, NV = 1 one half of it) times WT waves
+// along the rows, each wave holding NTB * 32 rows (2 * NTB blocks of 16).
+template <int NTB, int WT, int NV = 2>
 struct Tile {
-  static constexpr int NW = 2 * WT;            // waves per workgroup
+  static constexpr int NW = NV * WT;           // waves per workgroup
   static constexpr int NJ = 2 * NTB;           // row blocks of 16 per wave
   static constexpr int BT = WT * NTB * 32;     // rows per workgroup
+  static constexpr int TA = 128 * NV;          // A-tile rows per workgroup
+  static constexpr int kWB = TA * kRowBytes;
   static constexpr int kHBytes = BT * kRowBytes;
-  static constexpr int kStageBytes = kWBytes + kHBytes;
+  static constexpr int kStageBytes = kWB + kHBytes;
 };
 
 // Residency and pipeline depth of one kernel shape. Shapes whose wave holds
 // at most 128 x 64 accumulators (and no second accumulator set) run two
-// workgroups per CU when two stage buffers fit in half of the 160 KB LDS.
-template <int NTB, int WT, bool SPLITK4>
+// workgroups per CU when two stage buffers fit in half of the 160 KB LDS;
+// half-tile shapes (NV = 1) as many as fit with two buffers each, up to 3.
+template <int NTB, int WT, bool SPLITK4, int NV = 2>
 struct Shape {
-  using TL = Tile<NTB, WT>;
+  using TL = Tile<NTB, WT, NV>;
+  static constexpr int FIT2 = (160 * 1024) / (2 * TL::kStageBytes);
   static constexpr int PER_CU =
-      (WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1;
+      NV == 1 ? (FIT2 >= 3 ? 3 : FIT2)
+              : ((WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1);
   static constexpr int FIT = (160 * 1024 / PER_CU) / TL::kStageBytes;
   static constexpr int CAP = FIT < TIM_NBUF ? FIT : TIM_NBUF;
   // a power of two, so that it divides the stage count
@@ -189,30 +194,30 @@ struct TileOps {
 // Per-lane byte offsets of this wave's DMA loads, relative to the tile's
 // first row at hidden index 0. They do not change along the hidden dimension:
 // each stage only moves the scalar offset.
-template <int NTB, int WT>
+template <int NTB, int WT, int NV = 2>
 struct LoadPlan {
-  static constexpr int NW = Tile<NTB, WT>::NW;
-  static constexpr int WB = 4 * kChunks / NW;                         // W blocks of 1 KB per wave
-  static constexpr int HB = Tile<NTB, WT>::BT * kChunks / (64 * NW);  // hidden-state blocks per wave
+  static constexpr int NW = Tile<NTB, WT, NV>::NW;
+  static constexpr int WB = Tile<NTB, WT, NV>::TA * kChunks / (64 * NW);  // W blocks of 1 KB per wave
+  static constexpr int HB = Tile<NTB, WT, NV>::BT * kChunks / (64 * NW);  // hidden-state blocks per wave
   static constexpr int L = WB + HB;                                   // DMA loads per wave per stage
   uint32_t w_off[WB];
   uint32_t h_off[HB];
 };
 
-template <int NTB, int WT>
-__device__ __forceinline__ LoadPlan<NTB, WT> make_load_plan(int w_rows, int h_rows, int d, int wave, int lane) {
-  LoadPlan<NTB, WT> pl;
+template <int NTB, int WT, int NV = 2>
+__device__ __forceinline__ LoadPlan<NTB, WT, NV> make_load_plan(int w_rows, int h_rows, int d, int wave, int lane) {
+  LoadPlan<NTB, WT, NV> pl;
 #pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::WB; ++q) {
-    const int p = (wave * LoadPlan<NTB, WT>::WB + q) * 64 + lane;
+  for (int q = 0; q < LoadPlan<NTB, WT, NV>::WB; ++q) {
+    const int p = (wave * LoadPlan<NTB, WT, NV>::WB + q) * 64 + lane;
     int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
     if (r >= w_rows) r = w_rows - 1;  // rows past V: a valid row, masked in the epilogue
     pl.w_off[q] = (uint32_t)(r * d + c * 8) * 2u;
   }
 #pragma unroll
-  for (int q = 0; q < LoadPlan<NTB, WT>::HB; ++q) {
-    const int p = (wave * LoadPlan<NTB, WT>::HB + q) * 64 + lane;
+  for (int q = 0; q < LoadPlan<NTB, WT, NV>::HB; ++q) {
+    const int p = (wave * LoadPlan<NTB, WT, NV>::HB + q) * 64 + lane;
     int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
     if (r >= h_rows) r = h_rows - 1;  // rows past the batch: never written out
@@ -233,17 +238,18 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void* base, uint64_t bytes) {
 }
 
 // Load q of a stage request: the wave's L DMA loads of a stage, W blocks first.
-template <int NTB, int WT>
-__device__ __forceinline__ void request_load(unsigned char* buf, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl,
-                                             int wave, int soff, int q) {
+template <int NTB, int WT, int NV = 2>
+__device__ __forceinline__ void request_load(unsigned char* buf, rsrc_t wr, rsrc_t hr,
+                                             const LoadPlan<NTB, WT, NV>& pl, int wave, int soff, int q) {
 #if defined(__HIP_DEVICE_COMPILE__)
-  constexpr int WB = LoadPlan<NTB, WT>::WB;
-  constexpr int L = LoadPlan<NTB, WT>::L;
+  constexpr int WB = LoadPlan<NTB, WT, NV>::WB;
+  constexpr int L = LoadPlan<NTB, WT, NV>::L;
+  constexpr int kWB = Tile<NTB, WT, NV>::kWB;
   if (q < WB)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff, 0,
                                              TIM_LOAD_AUX);
   else
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWBytes + (wave * (L - WB) + (q - WB)) * 1024), 16,
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWB + (wave * (L - WB) + (q - WB)) * 1024), 16,
                                              pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
 #endif
 }
@@ -281,9 +287,9 @@ __device__ __forceinline__ bf16x8 read_a(const unsigned char* buf, int s, int bi
   return read_operand(buf, wv * 128 + bi * 16 + (lane & 15), s, lane);
 }
 // hidden-state block bj (16 rows) of row wave wt
-template <int NTB>
+template <int NTB, int NV = 2>
 __device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj, int wt, int lane) {
-  return read_operand(buf + kWBytes, wt * NTB * 32 + bj * 16 + (lane & 15), s, lane);
+  return read_operand(buf + 128 * NV * kRowBytes, wt * NTB * 32 + bj * 16 + (lane & 15), s, lane);
 }
 
 // One k-step as 8 * NJ scheduling units, each pinned on its own: unit i
@@ -296,13 +302,13 @@ __device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj
 // on; the W operands too with AD (then read right after the row blocks, so
 // every read lands early), else the single W set is refilled block by block
 // right after each block's last use here.
-template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true>
+template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true, int NV = 2>
 __device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
-                                      unsigned char* lb, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT>& pl, int soff,
-                                      const unsigned char* rb, int rs, int wave, int wv, int wt, int lane) {
+                                      unsigned char* lb, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT, NV>& pl,
+                                      int soff, const unsigned char* rb, int rs, int wave, int wv, int wt, int lane) {
   constexpr int NJ = 2 * NTB;
   constexpr int NM = 8 * NJ;
-  constexpr int L = LoadPlan<NTB, WT>::L;
+  constexpr int L = LoadPlan<NTB, WT, NV>::L;
   constexpr int PA = AD ? P : 0, PN = AD ? (P ^ 1) : 0;
   static_assert(L <= NM, "at most one DMA load per unit");
 #pragma unroll
@@ -311,10 +317,10 @@ __device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NT
     acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[PA][bi], fb[P][bj], acc[bi][bj], 0, 0, 0);
     if (LOAD) {  // load q goes with unit q * NM / L
       const int q = (i * L + NM - 1) / NM;
-      if (q < L && q * NM / L == i) request_load<NTB, WT>(lb, wr, hr, pl, wave, soff, q);
+      if (q < L && q * NM / L == i) request_load<NTB, WT, NV>(lb, wr, hr, pl, wave, soff, q);
     }
     if (READ) {
-      if (!AD && i < NJ) fb[P ^ 1][i] = read_b<NTB>(rb, rs, i, wt, lane);
+      if (!AD && i < NJ) fb[P ^ 1][i] = read_b<NTB, NV>(rb, rs, i, wt, lane);
       if (AD) {
         // NJ + 8 reads spread evenly over the units, in the order the next
         // k-step consumes them: a0, b0 .. b[NJ-1], a1 .. a7
@@ -322,7 +328,7 @@ __device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NT
         const int r = (i * NR + NM - 1) / NM;
         if (r < NR && r * NM / NR == i) {
           if (r == 0) fa[PN][0] = read_a(rb, rs, 0, wv, lane);
-          else if (r <= NJ) fb[P ^ 1][r - 1] = read_b<NTB>(rb, rs, r - 1, wt, lane);
+          else if (r <= NJ) fb[P ^ 1][r - 1] = read_b<NTB, NV>(rb, rs, r - 1, wt, lane);
           else fa[PN][r - NJ] = read_a(rb, rs, r - NJ, wv, lane);
         }
       } else {
@@ -346,30 +352,31 @@ __device__ __forceinline__ void quarter_fold(f32x4 (&acc)[8][2 * NTB], f32x4 (&s
       acc[bi][bj] = f32x4{};
     }
 }
-template <int NTB, int WT>
+template <int NTB, int WT, int NV = 2>
 struct TileCtx {
   int vt;
   int64_t v0, t0;
-  LoadPlan<NTB, WT> pl;
+  LoadPlan<NTB, WT, NV> pl;
   rsrc_t wr, hr, tr, cr;
 };
 
-template <int NTB, int WT, int GV>
-__device__ __forceinline__ TileCtx<NTB, WT> make_tile(const TileOps& o, int lid, int n_vt, int n_tt, int wave,
-                                                      int lane) {
-  constexpr int BT = Tile<NTB, WT>::BT;
+template <int NTB, int WT, int GV, int NV = 2>
+__device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int lid, int n_vt, int n_tt, int wave,
+                                                          int lane) {
+  constexpr int BT = Tile<NTB, WT, NV>::BT;
+  constexpr int TA = Tile<NTB, WT, NV>::TA;
   // Opaque copies: every call recomputes its context instead of the compiler
   // reusing (and keeping live) the result of an earlier call.
   asm volatile("" : "+s"(lid));
   asm volatile("" : "+v"(lane));
-  TileCtx<NTB, WT> c;
+  TileCtx<NTB, WT, NV> c;
   int tt;
   tile_of_lid<GV>(lid, n_vt, n_tt, c.vt, tt);
-  c.v0 = (int64_t)c.vt * kVocabTile;
+  c.v0 = (int64_t)c.vt * TA;
   c.t0 = (int64_t)tt * BT;
-  const int w_rows = (o.a_rows - c.v0) < kVocabTile ? (int)(o.a_rows - c.v0) : kVocabTile;
+  const int w_rows = (o.a_rows - c.v0) < TA ? (int)(o.a_rows - c.v0) : TA;
   const int h_rows = (o.b_rows - c.t0) < BT ? (int)(o.b_rows - c.t0) : BT;
-  c.pl = make_load_plan<NTB, WT>(w_rows, h_rows, o.K, wave, lane);
+  c.pl = make_load_plan<NTB, WT, NV>(w_rows, h_rows, o.K, wave, lane);
   c.wr = make_rsrc((const __bf16*)o.a + c.v0 * o.K, (uint64_t)w_rows * o.K * 2);
   c.hr = make_rsrc((const __bf16*)o.b + c.t0 * o.K, (uint64_t)h_rows * o.K * 2);
   c.tr = make_rsrc(o.tokens + c.t0, (uint64_t)h_rows * 4);
@@ -397,10 +404,12 @@ __device__ __forceinline__ TileCtx<NTB, WT> make_tile(const TileOps& o, int lid,
 // the stage requests; that only makes the later waits stricter.)
 template <int NTB, int WT, bool SPLITK4, class E>
 __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, int n_tt) {
-  using TL = Tile<NTB, WT>;
-  using LP = LoadPlan<NTB, WT>;
-  using TC = TileCtx<NTB, WT>;
-  constexpr int kNBuf = Shape<NTB, WT, SPLITK4>::NBUF;
+  constexpr int NV = E::kNV;
+  using TL = Tile<NTB, WT, NV>;
+  using LP = LoadPlan<NTB, WT, NV>;
+  using TC = TileCtx<NTB, WT, NV>;
+  using SH = Shape<NTB, WT, SPLITK4, NV>;
+  constexpr int kNBuf = SH::NBUF;
   static_assert((128 / kKS) % kNBuf == 0, "the stage count (a multiple of 128 / kKS) must be a multiple of kNBuf");
   constexpr int NJ = TL::NJ;
   constexpr int BT = TL::BT;
@@ -410,7 +419,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   constexpr int ROWB = (E::kTokens ? 2 * BT * 4 : 0) + (E::kCoef ? 2 * BT * 16 : 0);
   // Epilogue scratch of its own when it fits, so the next tile's stages can
   // land during the epilogue; otherwise it reuses the first stage buffer.
-  constexpr bool kSep = kNBuf * SB + EPI + ROWB <= (160 * 1024) / Shape<NTB, WT, SPLITK4>::PER_CU;
+  constexpr bool kSep = kNBuf * SB + EPI + ROWB <= (160 * 1024) / SH::PER_CU;
   // With its own scratch, the epilogue also finds the tile's per-row data
   // staged in LDS (two slots, alternating per tile), requested with the
   // tile's first stage, so it never waits on a global load behind the next
@@ -429,7 +438,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
 
   const int lane0 = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wv = wave & 1, wt = wave >> 1;
+  const int wv = NV == 2 ? (wave & 1) : 0, wt = wave / NV;
 
   // this workgroup's tiles: start + wi, start + wi + w_x, ... below start + t_x
   const int n_tiles = n_vt * n_tt;
@@ -445,7 +454,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   const int nk_q = nk / 4;     // stages per quarter (SPLITK4)
   constexpr int kStep = kKS * 2;
 
-  TC cur = make_tile<NTB, WT, E::kGroupA>(ops, start + j, n_vt, n_tt, wave, lane0);
+  TC cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, start + j, n_vt, n_tt, wave, lane0);
 
   // prologue: the tile's row data and stages 0 .. kNBuf - 1
   auto prologue = [&]() {
@@ -455,7 +464,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     for (int s = 0; s < kNBuf; ++s)
 #pragma unroll
       for (int q = 0; q < L; ++q)
-        request_load<NTB, WT>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q);
+        request_load<NTB, WT, NV>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q);
     wait_vmem<(kNBuf - 1) * L>();  // stage 0 (and the row data) landed
     __syncthreads();
   };
@@ -464,7 +473,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   f32x4 acc[8][NJ];
   f32x4 sum[8][SPLITK4 ? NJ : 1];
   // One wave per SIMD (four waves) leaves registers for a second A operand set.
-  constexpr bool kAD = TL::NW == 4 && Shape<NTB, WT, SPLITK4>::PER_CU == 1;
+  constexpr bool kAD = TL::NW == 4 && SH::PER_CU == 1;
   bf16x8 fa[2][8];   // A operands by k-step parity (with kAD), else fa[0] refilled in place
   bf16x8 fb[2][NJ];  // B operands, double buffered by k-step parity
   while (true) {
@@ -483,7 +492,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     // stage 0 has landed and is visible: after the prologue, or, when the
     // pipeline runs on from the previous tile, since its last boundary
 #pragma unroll
-    for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = read_b<NTB>(lds, 0, bj, wt, lane);
+    for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = read_b<NTB, NV>(lds, 0, bj, wt, lane);
 #pragma unroll
     for (int bi = 0; bi < 8; ++bi) fa[0][bi] = read_a(lds, 0, bi, wv, lane);
     int k = 0;
@@ -491,10 +500,10 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     for (; k + kNBuf < nk; ++k) {
       unsigned char* cb = lds + (k % kNBuf) * SB;
       region_a_prio();
-      kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
+      kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
       wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
+      kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
                                    lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
@@ -505,13 +514,13 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     // through the epilogue), to this tile's own stages again. Stage k sits in
     // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
     {
-      const TC nx = make_tile<NTB, WT, E::kGroupA>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
+      const TC nx = make_tile<NTB, WT, E::kGroupA, NV>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
 #pragma unroll
       for (int t = 0; t < kNBuf; ++t) {
         k = nk - kNBuf + t;
         unsigned char* cb = lds + t * SB;
         region_a_prio();
-        kstep<NTB, WT, 0, kAD, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
+        kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
         wait_lgkm0_vmem<(kNBuf - 2) * L>();
         stage_barrier();
         // request k + kNBuf: stage t of the next tile (with its row data)
@@ -520,10 +529,10 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
           if constexpr (kTokLds) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
         }
         if (t + 1 < kNBuf)
-          kstep<NTB, WT, 1, kAD, true>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
+          kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
                                        wave, wv, wt, lane);
         else
-          kstep<NTB, WT, 1, kAD, true, false>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
+          kstep<NTB, WT, 1, kAD, true, false, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
                                               wt, lane);
         if constexpr (SPLITK4) {
           if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
@@ -546,7 +555,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     par ^= 1;
     if (!has_next) break;
     j += w_x;
-    cur = make_tile<NTB, WT, E::kGroupA>(ops, next_lid, n_vt, n_tt, wave, lane);
+    cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, next_lid, n_vt, n_tt, wave, lane);
     if constexpr (!kSep) {
       __syncthreads();  // the epilogue's reads of the first buffer are done
       prologue();

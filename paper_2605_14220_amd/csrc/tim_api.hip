@@ -2,8 +2,10 @@
 //
 // The planner only chooses launch shapes. Rollout mode sends the whole ragged
 // batch in one launch with a row tile sized to the batch (64, 128 or 256 rows
-// per workgroup); training mode walks the packed stream in micro-batches with
-// 256-row tiles. Every shape runs the same per-row instruction sequence.
+// per workgroup; a batch of at most 64 rows may take half vocabulary tiles,
+// three workgroups per CU, where they fill the chip's rounds more evenly);
+// training mode walks the packed stream in micro-batches with 256-row tiles.
+// Every shape runs the same per-row instruction sequence.
 
 #include <hip/hip_runtime.h>
 
@@ -50,6 +52,7 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
   const bool splitk4 = order == TIM_ORDER_SPLITK4;
   const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
   const int tb = row_tile_for(step, mode, splitk4);
+  const bool halves = !splitk4 && tim::uses_half_tiles(step, mode) && tim::prefer_half_tiles(V);
   const float inv_tau = inv_temperature(temperature);
   const __bf16* h = (const __bf16*)hidden;
   tim::Partial* part = (tim::Partial*)workspace;
@@ -66,11 +69,17 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
     a.inv_tau = inv_tau;
     a.part = part;
     a.logits = nullptr;
-    st = hip_status(tim::launch_partials(a, tb, splitk4, stream));
-    if (st != TIM_OK) return st;
-    st = hip_status(tim::launch_merge(part, tokens + t0, rows, V, splitk4, logp + t0,
-                                      entropy ? entropy + t0 : nullptr, lse ? lse + t0 : nullptr,
-                                      stream));
+    float* ent = entropy ? entropy + t0 : nullptr;
+    float* ls = lse ? lse + t0 : nullptr;
+    if (halves) {
+      st = hip_status(tim::launch_partials_halves(a, stream));
+      if (st != TIM_OK) return st;
+      st = hip_status(tim::launch_merge_halves(part, tokens + t0, rows, V, logp + t0, ent, ls, stream));
+    } else {
+      st = hip_status(tim::launch_partials(a, tb, splitk4, stream));
+      if (st != TIM_OK) return st;
+      st = hip_status(tim::launch_merge(part, tokens + t0, rows, V, splitk4, logp + t0, ent, ls, stream));
+    }
     if (st != TIM_OK) return st;
   }
   return TIM_OK;

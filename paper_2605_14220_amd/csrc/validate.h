@@ -13,6 +13,7 @@ namespace tim {
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 inline int n_tiles_of(int32_t V) { return (int)((V + TIM_VOCAB_TILE - 1) / TIM_VOCAB_TILE); }
+inline int n_half_tiles_of(int32_t V) { return (int)((V + TIM_VOCAB_TILE / 2 - 1) / (TIM_VOCAB_TILE / 2)); }
 
 // Shape/value checks shared by tim_logprobs, tim_logits and the workspace query.
 inline tim_status check_shape(int64_t T, int32_t d, int32_t V, int32_t order) {
@@ -33,8 +34,15 @@ inline int64_t rows_per_launch(int64_t T, int32_t mode, int64_t micro_batch) {
   return T;
 }
 
+// Rollout launches of at most this many rows (decode batches) may form their
+// partials over half vocabulary tiles; their workspace covers that case.
+constexpr int64_t kHalfTileRows = 64;
+inline bool uses_half_tiles(int64_t rows, int32_t mode) { return mode == TIM_MODE_ROLLOUT && rows <= kHalfTileRows; }
+
 inline size_t workspace_bytes(int64_t T, int32_t V, int32_t mode, int64_t micro_batch) {
-  return (size_t)rows_per_launch(T, mode, micro_batch) * (size_t)n_tiles_of(V) * 16u;
+  const int64_t rows = rows_per_launch(T, mode, micro_batch);
+  const int per_row = uses_half_tiles(rows, mode) ? n_half_tiles_of(V) : n_tiles_of(V);
+  return (size_t)rows * (size_t)per_row * 16u;
 }
 
 inline tim_status validate_logprobs(const void* hidden, const void* w, const int32_t* tokens,

@@ -64,12 +64,17 @@ def test_status_strings(lib):
     (147000, 4096, 151936, Mode.TRAINING, 16384),
     (147000, 4096, 151936, Mode.TRAINING, 200000),
     (200, 4096, 151936, Mode.ROLLOUT, 16384),
+    (65, 4096, 151936, Mode.ROLLOUT, 0),
+    (64, 4096, 151936, Mode.ROLLOUT, 0),
     (5, 128, 1, Mode.ROLLOUT, 0),
+    (7, 128, 4096 + 129, Mode.ROLLOUT, 0),
     (131072, 5120, 152064, Mode.TRAINING, 32768),
 ])
 def test_workspace_size_formula(lib, T, d, V, mode, mb):
     rows = T if (mode == Mode.ROLLOUT or mb == 0 or mb >= T) else mb
-    assert tim.workspace_size(T, d, V, mode, mb) == rows * math.ceil(V / 256) * 16
+    # decode batches (rollout, at most 64 rows) keep one partial per half tile
+    width = 128 if (mode == Mode.ROLLOUT and rows <= 64) else 256
+    assert tim.workspace_size(T, d, V, mode, mb) == rows * math.ceil(V / width) * 16
 
 
 @pytest.mark.parametrize("args", [(0, 256, 4096, 1, 0), (-1, 256, 4096, 1, 0), (10, 100, 4096, 1, 0),
@@ -119,6 +124,7 @@ def test_logprobs_T_zero_is_noop_even_with_null_pointers(lib):
     (dict(ws_bytes=8 * 16 * 16 - 1), Status.ERR_WORKSPACE),
     (dict(ws_bytes=0), Status.ERR_WORKSPACE),
     (dict(T=100, mb=10, ws_bytes=10 * 16 * 16 - 16), Status.ERR_WORKSPACE),
+    (dict(mode=0, ws_bytes=8 * 32 * 16 - 1), Status.ERR_WORKSPACE),
 ])
 def test_logprobs_rejects(lib, kw, expect):
     assert _lp(lib, **kw) == expect
