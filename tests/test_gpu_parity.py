@@ -162,3 +162,20 @@ def test_splitk4_engine_matches_oracle_but_not_bits():
     za = tim.logits(h, W, 1.0)
     assert not torch.equal(za, zb)
     check_close("splitk4 logits", zb.flatten(), za.double().cpu().flatten(), 1e-4)
+
+
+@pytest.mark.parametrize("V,mode", [(4096, Mode.TRAINING), (1000, Mode.TRAINING), (4096, Mode.ROLLOUT),
+                                    (151936, Mode.ROLLOUT)])
+def test_duplicated_vocabulary_shifts_by_log2(V, mode):
+    """W -> [W; W] with every token in the first copy: each logit appears
+    twice, so the normaliser doubles: logp drops by ln 2 and the entropy rises
+    by ln 2 (with 2^k tiles per copy the two copies' subtrees are the same
+    partials and the shift is exact up to the final log)."""
+    T, d = 64, 256
+    h, W = inputs(T, d, V, seed=V % 101, w_std=0.1)
+    tok = random_tokens(T, V, seed=V % 101)
+    W2 = torch.cat([W, W]).contiguous()
+    lp, H, _ = tim.logprobs(h, W, tok, 1.0, mode=mode)
+    lp2, H2, _ = tim.logprobs(h, W2, tok, 1.0, mode=mode)
+    check_close(f"dup logp V={V}", lp2, (lp.double() - math.log(2)).cpu().numpy(), 5e-6)
+    check_close(f"dup entropy V={V}", H2, (H.double() + math.log(2)).cpu().numpy(), 2e-5)
