@@ -22,9 +22,13 @@
 //   the sampled token's logit from the same register value. Logits never
 //   reach HBM.
 //
-// Kernel 2, lmhead_merge: one wavefront per row merges that row's partials with
-//   a fixed balanced binary tree over the tile index, then
-//   logp = z_tok - (M + log S) and H = log S - U / S.
+// Decode batches may run lmhead_half_partials instead: the same pass over
+//   128-entry halves of the vocab tiles, writing each half's partial where
+//   the whole-tile epilogue merges the two; the merge pairs them up again.
+//
+// Kernel 2, lmhead_merge: one wavefront per row (four for launches of at most
+//   512 rows) merges that row's partials with a fixed balanced binary tree
+//   over the tile index, then logp = z_tok - (M + log S) and H = log S - U / S.
 //
 // Reduction structure inside one vocab tile, for one row (fixed): each of the
 // two vocab waves holds 128 entries of the row, 32 per lane in 4 lanes; per

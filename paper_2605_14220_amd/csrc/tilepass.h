@@ -3,7 +3,8 @@
 //
 // A pass computes output tiles C[i][j] = sum_k A[i][k] B[j][k] over two
 // bf16 row-major operands with K contiguous (A [a_rows, K] in tiles of 256
-// rows, B [b_rows, K] in tiles of the workgroup's row tile) on
+// rows, or 128 for the half-tile shape of decode batches, B [b_rows, K] in
+// tiles of the workgroup's row tile) on
 // v_mfma_f32_16x16x32_bf16 with fp32 accumulation, K in ascending 32-element
 // steps and one accumulation chain per output element: an element's value
 // depends only on its own A row, B row and K, never on how many rows share a
@@ -63,7 +64,6 @@ constexpr int kRowBytes = kKS * 2;       // bytes of one row in one stage
 constexpr int kChunks = kRowBytes / 16;  // 16-byte chunks per row per stage
 constexpr int kKM = 32;                  // hidden-dimension elements per MFMA
 constexpr int kSteps = kKS / kKM;        // MFMA k-steps per stage
-constexpr int kWBytes = kVocabTile * kRowBytes;
 static_assert(kSteps == 2, "the operand double buffer alternates once per k-step");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_inff();
@@ -179,8 +179,9 @@ __device__ __forceinline__ void tile_of_lid(int lid, int n_vt, int n_tt, int& vt
 }
 
 // Operands of one tile pass, C[i][j] = sum_k A[i][k] B[j][k] over A [a_rows, K]
-// and B [b_rows, K], bf16, row-major with row stride K. The A tile is 256 rows
-// (the vocabulary tile of the LM head) and the B tile the workgroup's row tile.
+// and B [b_rows, K], bf16, row-major with row stride K. The A tile is 128 NV
+// rows (256: the vocabulary tile of the LM head) and the B tile the
+// workgroup's row tile.
 struct TileOps {
   const void* a;
   const void* b;
