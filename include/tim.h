@@ -70,7 +70,7 @@ typedef enum {
 /* Bytes of device workspace tim_logprobs needs for these arguments:
  * rows_per_launch * ceil(V / TIM_VOCAB_TILE) * 16, where rows_per_launch is T
  * in rollout mode and min(T, micro_batch) in training mode (micro_batch 0 means
- * T); in rollout mode with T <= 64 (a decode batch, whose partials may be
+ * T); in rollout mode with T <= 128 (a decode batch, whose partials may be
  * taken over half tiles) T * ceil(V / (TIM_VOCAB_TILE / 2)) * 16. Returns 0 for
  * invalid arguments or T == 0. Pure host function. */
 size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch);
@@ -100,7 +100,7 @@ size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode
  * TIM_VOCAB_TILE vocabulary entries, each the merge of its two halves' (lower
  * half first); partials merged by a fixed balanced tree over the tile index.
  * None of this depends on T, mode, micro_batch or a row's position in the
- * batch (a decode batch of at most 64 rows may write the halves' partials
+ * batch (a decode batch of at most 128 rows may write the halves' partials
  * and merge each pair in the merge pass, which gives the same bits), so with
  * TIM_ORDER_INVARIANT a row's outputs are bitwise identical however it is
  * batched. NaN or Inf in the inputs

@@ -68,17 +68,19 @@ int n_half_tiles(int V);
 // Partials of every (row, vocab tile). rows_per_wg in {64, 128, 256} is the
 // row tile of one workgroup; it changes the launch shape only.
 hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, hipStream_t s);
-// Partials of every (row, half vocabulary tile) of up to 64 rows per row
-// tile: part is [rows, n_half_tiles]; each half's partial equals the one the
-// whole-tile epilogue merges, so launch_merge_halves gives the outputs of
-// launch_partials + launch_merge bit for bit.
+// Partials of every (row, half vocabulary tile), 64 or 128 rows per row tile
+// (by the launch's row count): part is [rows, n_half_tiles]; each half's
+// partial equals the one the whole-tile epilogue merges, so
+// launch_merge_halves gives the outputs of launch_partials + launch_merge bit
+// for bit.
 hipError_t launch_partials_halves(const LmHeadArgs& a, hipStream_t s);
-// Whether a decode batch on the current device takes half tiles: the shape
-// (whole tiles two per CU, or half tiles three per CU) whose last round of
-// workgroups leaves fewer slots idle. Either gives the same bits; the half
-// shape re-reads the row tile once per 128 vocabulary entries instead of 256,
-// so it only pays where it evens out the rounds.
-bool prefer_half_tiles(int V);
+// Whether a decode batch of `rows` rows on the current device takes half
+// tiles. Up to 64 rows: the shape (whole tiles two per CU, or half tiles
+// three per CU) whose last round of workgroups leaves fewer slots idle; the
+// half shape re-reads the row tile once per 128 vocabulary entries instead of
+// 256, so it only pays where it evens out the rounds. 65..128 rows: always
+// (whole tiles one per CU against halves two). Either gives the same bits.
+bool prefer_half_tiles(int V, int64_t rows);
 hipError_t launch_merge_halves(const Partial* part, const int32_t* tokens, int64_t rows, int V, float* logp,
                                float* entropy, float* lse, hipStream_t s);
 // Fixed-order merge of each row's partials into logp / entropy / lse.

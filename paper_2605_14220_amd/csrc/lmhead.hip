@@ -433,7 +433,10 @@ static double round_fill(int64_t units, int64_t slots) {
   return (double)units / (double)(rounds * slots);
 }
 
-bool prefer_half_tiles(int V) {
+bool prefer_half_tiles(int V, int64_t rows) {
+  // 65..128 rows: whole tiles of this row tile run one workgroup per CU,
+  // halves two, which measured faster at every vocabulary size tried
+  if (rows > 64) return true;
   const int cus = device_cu_count();
   if (cus <= 0) return false;
   const int64_t whole_slots = (int64_t)cus * Shape<1, 2, false>::PER_CU;
@@ -441,14 +444,21 @@ bool prefer_half_tiles(int V) {
   return round_fill(n_half_tiles(V), half_slots) > round_fill(n_vocab_tiles(V), whole_slots);
 }
 
-hipError_t launch_partials_halves(const LmHeadArgs& a, hipStream_t s) {
+template <int NTB>
+static hipError_t launch_halves_t(const LmHeadArgs& a, hipStream_t s) {
   const int n_ht = n_half_tiles(a.V);
-  constexpr int BT = Tile<1, 2, 1>::BT;
+  constexpr int BT = Tile<NTB, 2, 1>::BT;
   const int64_t n_tt = (a.rows + BT - 1) / BT;
   const int64_t nblk = n_tt * n_ht;
   if (nblk > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((lmhead_half_partials<1, 2>), dim3((unsigned)nblk), dim3(64 * 2), 0, s, a, n_ht, (int)n_tt);
+  hipLaunchKernelGGL((lmhead_half_partials<NTB, 2>), dim3((unsigned)nblk), dim3(64 * 2), 0, s, a, n_ht, (int)n_tt);
   return hipGetLastError();
+}
+
+// 64-row tiles (three workgroups of 2 waves per CU) up to 64 rows, 128-row
+// tiles (two per CU) above.
+hipError_t launch_partials_halves(const LmHeadArgs& a, hipStream_t s) {
+  return a.rows <= 64 ? launch_halves_t<1>(a, s) : launch_halves_t<2>(a, s);
 }
 
 // Launches of at most this many rows merge with four waves per row.

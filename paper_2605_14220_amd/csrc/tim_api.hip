@@ -2,8 +2,8 @@
 //
 // The planner only chooses launch shapes. Rollout mode sends the whole ragged
 // batch in one launch with a row tile sized to the batch (64, 128 or 256 rows
-// per workgroup; a batch of at most 64 rows may take half vocabulary tiles,
-// three workgroups per CU, where they fill the chip's rounds more evenly);
+// per workgroup; a batch of at most 128 rows may take half vocabulary tiles,
+// which run more workgroups per CU);
 // training mode walks the packed stream in micro-batches with 256-row tiles.
 // Every shape runs the same per-row instruction sequence.
 
@@ -52,7 +52,7 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
   const bool splitk4 = order == TIM_ORDER_SPLITK4;
   const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
   const int tb = row_tile_for(step, mode, splitk4);
-  const bool halves = !splitk4 && tim::uses_half_tiles(step, mode) && tim::prefer_half_tiles(V);
+  const bool halves = !splitk4 && tim::uses_half_tiles(step, mode) && tim::prefer_half_tiles(V, step);
   const float inv_tau = inv_temperature(temperature);
   const __bf16* h = (const __bf16*)hidden;
   tim::Partial* part = (tim::Partial*)workspace;

@@ -36,7 +36,7 @@ inline int64_t rows_per_launch(int64_t T, int32_t mode, int64_t micro_batch) {
 
 // Rollout launches of at most this many rows (decode batches) may form their
 // partials over half vocabulary tiles; their workspace covers that case.
-constexpr int64_t kHalfTileRows = 64;
+constexpr int64_t kHalfTileRows = 128;
 inline bool uses_half_tiles(int64_t rows, int32_t mode) { return mode == TIM_MODE_ROLLOUT && rows <= kHalfTileRows; }
 
 inline size_t workspace_bytes(int64_t T, int32_t V, int32_t mode, int64_t micro_batch) {

@@ -64,7 +64,8 @@ def test_status_strings(lib):
     (147000, 4096, 151936, Mode.TRAINING, 16384),
     (147000, 4096, 151936, Mode.TRAINING, 200000),
     (200, 4096, 151936, Mode.ROLLOUT, 16384),
-    (65, 4096, 151936, Mode.ROLLOUT, 0),
+    (129, 4096, 151936, Mode.ROLLOUT, 0),
+    (128, 4096, 151936, Mode.ROLLOUT, 0),
     (64, 4096, 151936, Mode.ROLLOUT, 0),
     (5, 128, 1, Mode.ROLLOUT, 0),
     (7, 128, 4096 + 129, Mode.ROLLOUT, 0),
@@ -72,8 +73,8 @@ def test_status_strings(lib):
 ])
 def test_workspace_size_formula(lib, T, d, V, mode, mb):
     rows = T if (mode == Mode.ROLLOUT or mb == 0 or mb >= T) else mb
-    # decode batches (rollout, at most 64 rows) keep one partial per half tile
-    width = 128 if (mode == Mode.ROLLOUT and rows <= 64) else 256
+    # decode batches (rollout, at most 128 rows) keep one partial per half tile
+    width = 128 if (mode == Mode.ROLLOUT and rows <= 128) else 256
     assert tim.workspace_size(T, d, V, mode, mb) == rows * math.ceil(V / width) * 16
 
 
