@@ -92,6 +92,99 @@ def cpu_baseline(h, W, tok, tau, rows: int, seed: int = 7):
     return idx, lp, ent, dt, threads
 
 
+def _threads():
+    from threadpoolctl import threadpool_info
+    return int(max([p.get("num_threads", 1) for p in threadpool_info()] or [1]))
+
+
+def oracle_beside(dev, T, tau, cu, adv, norm_sample, bwd_sample, W):
+    """The oracle timed beside the other rows of the path, each on inputs that
+    are seeded and synthetic (never the path's outputs), with the largest
+    GPU - oracle difference on the same inputs:
+    * mismatch, sequence statistics and PPO loss over the whole packed stream
+      of seeded log-prob pairs (trainer / rollout) of the workload's shape;
+    * the final RMS norm and its gradients on sampled rows of the hidden states;
+    * grad_hidden of the backward on sampled rows (each depends on its row only)."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2605_14220_amd as tim
+    from oracle.logprobs import bf16_to_f64
+    from workload import bf16_bits, logprob_pairs
+
+    thr = _threads()
+    res = {}
+
+    def timed(fn):
+        t0 = time.perf_counter()
+        r = fn()
+        return r, time.perf_counter() - t0
+
+    a_np, b_np = logprob_pairs(T, seed=71)
+    a_t, b_t = torch.from_numpy(a_np).to(dev), torch.from_numpy(b_np).to(dev)
+    cu_np = cu.cpu().numpy()
+    sample = f"the whole {T}-token packed stream of seeded log-prob pairs (workload.logprob_pairs, seed 71)"
+
+    (lr_r, k3_r, w_r), dt = timed(lambda: oracle.mismatch(a_np, b_np, 2.0))
+    lr_g, k3_g, w_g = (x.double().cpu().numpy() for x in tim.mismatch(a_t, b_t, 2.0))
+    res["mismatch"] = {
+        "cpu_oracle": {"value": T / dt, "unit": "tokens/s", "cores": thr, "kind": "oracle", "sample": sample},
+        "oracle_parity": {"max_abs_dlog_ratio": float(np.abs(lr_g - lr_r).max()),
+                          "max_abs_dk3": float(np.abs(k3_g - k3_r).max()),
+                          "max_rel_dis_weight": float((np.abs(w_g - w_r) / w_r).max())}}
+
+    (sc_r, keep_r, ws_r), dt = timed(lambda: oracle.mismatch_seq(a_np, b_np, cu_np, "k3", 2.0, 1e-3))
+    sc_g, keep_g, ws_g = tim.mismatch_seq(a_t, b_t, cu, C=2.0, tau_seq=1e-3)
+    res["seq"] = {
+        "cpu_oracle": {"value": T / dt, "unit": "tokens/s", "cores": thr, "kind": "oracle", "sample": sample},
+        "oracle_parity": {"max_rel_dscore": float(np.abs(sc_g.cpu().numpy() - sc_r).max() / np.abs(sc_r).max()),
+                          "keep_masks_equal": bool(np.array_equal(keep_g.cpu().numpy().astype(bool), keep_r)),
+                          "max_abs_dweight": float(np.abs(ws_g.double().cpu().numpy() - ws_r).max())}}
+
+    w32 = w_r.astype(np.float32)  # the oracle's own truncated token weights
+    adv_np = adv.cpu().numpy()
+    pr, dt = timed(lambda: oracle.ppo_loss(a_np, b_np, adv_np, cu_np, 0.2, 0.28, weight=w32))
+    pg = tim.ppo_loss(a_t, b_t, adv, cu, 0.2, 0.28, torch.from_numpy(w32).to(dev))
+    res["ppo"] = {
+        "cpu_oracle": {"value": T / dt, "unit": "tokens/s", "cores": thr, "kind": "oracle",
+                       "sample": sample + ", seeded advantages, the oracle's own truncated IS weights"},
+        "oracle_parity": {"rel_dbatch_loss": float(abs(float(pg["batch_loss"].item()) - pr["batch_loss"])
+                                                   / max(abs(pr["batch_loss"]), 1e-300)),
+                          "max_abs_dgrad": float(np.abs(pg["grad"].double().cpu().numpy() - pr["grad"]).max()),
+                          "clipped_equal": bool(np.array_equal(pg["clipped"].cpu().numpy().astype(bool),
+                                                               pr["clipped"]))}}
+
+    if norm_sample is not None:
+        idx, x_bits, g_bits, G, h_gpu, gx_gpu = norm_sample
+        (hb_r, _, _), dt_f = timed(lambda: oracle.rmsnorm(x_bits, g_bits, 1e-6))
+        (dx_r, _), dt_b = timed(lambda: oracle.rmsnorm_grads(x_bits, g_bits, 1e-6, G))
+        code_diff = np.abs(h_gpu.astype(np.int32) - hb_r.astype(np.int32))
+        res["rmsnorm"] = {
+            "cpu_oracle": {"value": len(idx) / (dt_f + dt_b), "unit": "rows/s (forward + backward)", "cores": thr,
+                           "kind": "oracle", "sample": f"{len(idx)} seeded rows (seed 72) of the hidden states"},
+            "oracle_parity": {"codes_equal_frac": float((code_diff == 0).mean()),
+                              "max_code_diff": int(code_diff.max()),
+                              "max_rel_dgrad_x": float(np.abs(gx_gpu - dx_r).max() / np.abs(dx_r).max())}}
+
+    if bwd_sample is not None:
+        idx, h_bits, tok_np, g_lp, g_h, gh_gpu = bwd_sample
+        w_bits = bf16_bits(W)
+
+        def grad_hidden():
+            dacc = oracle.logit_grads(h_bits, w_bits, tok_np, tau, g_lp, g_h)
+            dh = np.zeros((len(idx), w_bits.shape[1]))
+            for v0 in range(0, w_bits.shape[0], 8192):  # dacc . W over vocabulary chunks (bounded memory)
+                dh += dacc[:, v0:v0 + 8192] @ bf16_to_f64(w_bits[v0:v0 + 8192])
+            return dh
+        dh_r, dt = timed(grad_hidden)
+        res["backward"] = {
+            "cpu_oracle": {"value": len(idx) / dt, "unit": "tokens/s (grad_hidden rows)", "cores": thr,
+                           "kind": "oracle", "sample": f"grad_hidden of {len(idx)} seeded rows (seed 73)"},
+            "oracle_parity": {"max_rel_dgrad_hidden": float(np.abs(gh_gpu - dh_r).max() / np.abs(dh_r).max())}}
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -303,6 +396,13 @@ def main(argv=None):
     n1.record(stream)
     torch.cuda.synchronize()
     nb_ms = n0.elapsed_time(n1) / 5
+    norm_sample = None
+    if args.cpu_rows > 0:
+        from workload import bf16_bits
+        idx_n = np.sort(np.random.default_rng(72).choice(T, size=min(2048, T), replace=False))
+        it_n = torch.as_tensor(idx_n, device=dev)
+        norm_sample = (idx_n, bf16_bits(h.index_select(0, it_n)), bf16_bits(gam), G_n.index_select(0, it_n).double().cpu().numpy(),
+                       bf16_bits(h_n.index_select(0, it_n)), gx_n.index_select(0, it_n).double().cpu().numpy())
     nf_bytes = 4.0 * T * d + 4.0 * T
     nb_bytes = 16.0 * T * d
     norm = {"forward_ms": nf_ms, "forward_GBps": nf_bytes / (nf_ms / 1e3) / 1e9,
@@ -317,6 +417,7 @@ def main(argv=None):
 
     # backward of the fused log-prob over the whole stream (the trainer's gradients)
     bwd = None
+    bwd_sample = None
     if args.backward:
         g = torch.Generator(device="cpu").manual_seed(99)
         g_lp = torch.randn(T, generator=g).to(dev)
@@ -346,6 +447,14 @@ def main(argv=None):
                "finite": bool(torch.isfinite(gh).all().item() and torch.isfinite(gw).all().item())}
         log(f"[bench] backward over {T} tokens (micro-batch {mb}): {b_ms:.1f} ms/call, {bwd['tokens_per_s']:,.0f} "
             f"tokens/s, {bwd['achieved']:.1f} TFLOP/s = {bwd['frac']:.1%} of bf16 peak (3 contractions)")
+        if args.cpu_rows > 0:
+            from workload import bf16_bits
+            idx_b = np.sort(np.random.default_rng(73).choice(T, size=4, replace=False))
+            it_b = torch.as_tensor(idx_b, device=dev)
+            bwd_sample = (idx_b, bf16_bits(h.index_select(0, it_b)), tok.index_select(0, it_b).cpu().numpy(),
+                          g_lp.index_select(0, it_b).double().cpu().numpy(),
+                          g_h.index_select(0, it_b).double().cpu().numpy(),
+                          gh.index_select(0, it_b).double().cpu().numpy())
         del bws, gw, gh
         torch.cuda.empty_cache()
 
@@ -358,6 +467,7 @@ def main(argv=None):
 
     cpu = None
     parity = None
+    mstats = None
     if args.cpu_rows > 0:
         log(f"[bench] oracle CPU baseline on {args.cpu_rows} sampled rows ...")
         idx, lp_ref, ent_ref, dt, threads = cpu_baseline(h, W, tok, tau, args.cpu_rows)
@@ -370,6 +480,15 @@ def main(argv=None):
         parity = {"rows": int(args.cpu_rows), "max_abs_dlogp": e_lp, "max_abs_dentropy": e_h}
         log(f"[bench] oracle: {cpu['value']:.1f} tokens/s on {threads} threads; parity on sample: "
             f"max|dlogp|={e_lp:.2e} max|dH|={e_h:.2e}")
+        log("[bench] oracle beside the other rows ...")
+        beside = oracle_beside(dev, T, tau, cu, adv, norm_sample, bwd_sample, W)
+        for key, obj in (("mismatch", None), ("seq", seq), ("ppo", ppo), ("rmsnorm", norm), ("backward", bwd)):
+            if key in beside and obj is not None:
+                obj.update(beside[key])
+        mstats = beside.get("mismatch")
+        log("[bench] oracle beside: " + "; ".join(
+            f"{k} {v['cpu_oracle']['value']:.3g} {v['cpu_oracle']['unit']} parity {v['oracle_parity']}"
+            for k, v in beside.items()))
 
     out = {
         "metric": METRIC,
@@ -395,6 +514,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "parity_sample": parity,
         "mismatch_vs_splitk4": mis,
+        "mismatch_stats": mstats,
         "rollout_decode": rollout,
         "sequence_mismatch": seq,
         "backward": bwd,
