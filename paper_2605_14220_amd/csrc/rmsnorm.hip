@@ -37,31 +37,47 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// The row's squares summed into `acc` in the fixed lane order (chunk by
+// chunk, the 8 elements of a chunk in order).
+__device__ __forceinline__ float sum_squares(uint4 v, float acc) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a = bf16_lo(w[i]), b = bf16_hi(w[i]);
+    acc = __builtin_fmaf(a, a, acc);
+    acc = __builtin_fmaf(b, b, acc);
+  }
+  return acc;
+}
+
+// NCL > 0: d = 512 NCL, and a lane keeps its NCL chunks of the row in
+// registers between the two passes (all loads issued up front); NCL = 0: any
+// d, the row read again for the second pass. The arithmetic is the same.
+template <int NCL>
 __global__ __launch_bounds__(256) void rmsnorm_fwd(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
                                                    int64_t T, int d, float eps, uint4* __restrict__ h,
                                                    float* __restrict__ rstd) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const int nc = d / 8;
+  const int nc = NCL > 0 ? NCL * 64 : d / 8;
   const uint4* xr = x + t * nc;
+  uint4 xv[NCL > 0 ? NCL : 1];
   float acc = 0.f;
-  for (int c = lane; c < nc; c += 64) {
-    const uint4 v = xr[c];
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  if constexpr (NCL > 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float a = bf16_lo(w[i]), b = bf16_hi(w[i]);
-      acc = __builtin_fmaf(a, a, acc);
-      acc = __builtin_fmaf(b, b, acc);
-    }
+    for (int i = 0; i < NCL; ++i) xv[i] = xr[lane + 64 * i];
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) acc = sum_squares(xv[i], acc);
+  } else {
+    for (int c = lane; c < nc; c += 64) acc = sum_squares(xr[c], acc);
   }
   const float var = wave_sum(acc) / (float)d;
   const float r = 1.0f / __builtin_sqrtf(var + eps);
   if (rstd && lane == 0) rstd[t] = r;
   uint4* hr = h + t * nc;
-  for (int c = lane; c < nc; c += 64) {
-    const uint4 v = xr[c];
+  // h = bf16(g * bf16(x r)) for chunk c of the row
+  auto out_chunk = [&](int c, uint4 v) {
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
     uint32_t g[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
     if (gamma) {
@@ -80,49 +96,70 @@ __global__ __launch_bounds__(256) void rmsnorm_fwd(const uint4* __restrict__ x, 
       o[i] = (uint32_t)to_bf16(lo) | ((uint32_t)to_bf16(hi) << 16);
     }
     hr[c] = uint4{o[0], o[1], o[2], o[3]};
+  };
+  if constexpr (NCL > 0) {
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) out_chunk(lane + 64 * i, xv[i]);
+  } else {
+    for (int c = lane; c < nc; c += 64) out_chunk(c, xr[c]);
   }
 }
 
+// gamma's chunk c as 4 packed pairs (1.0 without a weight)
+__device__ __forceinline__ uint4 gamma_chunk(const uint4* __restrict__ gamma, int c) {
+  return gamma ? gamma[c] : uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
+}
+
+// Same two-mode structure as the forward (NCL > 0: the row's x, G and gamma
+// chunks kept in registers between the passes).
+template <int NCL>
 __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
                                                      const float* __restrict__ rstd, const float4* __restrict__ G,
                                                      int64_t T, int d, float4* __restrict__ dx) {
   const int lane = threadIdx.x & 63;
   const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;
-  const int nc = d / 8;
+  const int nc = NCL > 0 ? NCL * 64 : d / 8;
   const uint4* xr = x + t * nc;
   const float4* gr = G + t * (int64_t)(d / 4);
-  float acc = 0.f;
-  for (int c = lane; c < nc; c += 64) {
-    const uint4 v = xr[c];
-    const float4 g0 = gr[2 * c], g1 = gr[2 * c + 1];
+  // s += G g x over chunk c, in element order
+  auto dot_chunk = [](uint4 v, float4 g0, float4 g1, uint4 gv, float acc) {
     const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t gm[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
-    if (gamma) {
-      const uint4 gv = gamma[c];
-      gm[0] = gv.x, gm[1] = gv.y, gm[2] = gv.z, gm[3] = gv.w;
-    }
+    const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       acc = __builtin_fmaf(gg[2 * i] * bf16_lo(gm[i]), bf16_lo(w[i]), acc);
       acc = __builtin_fmaf(gg[2 * i + 1] * bf16_hi(gm[i]), bf16_hi(w[i]), acc);
     }
+    return acc;
+  };
+  uint4 xv[NCL > 0 ? NCL : 1], gmv[NCL > 0 ? NCL : 1];
+  float4 g0v[NCL > 0 ? NCL : 1], g1v[NCL > 0 ? NCL : 1];
+  float acc = 0.f;
+  if constexpr (NCL > 0) {
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) {
+      const int c = lane + 64 * i;
+      xv[i] = xr[c];
+      g0v[i] = gr[2 * c];
+      g1v[i] = gr[2 * c + 1];
+      gmv[i] = gamma_chunk(gamma, c);
+    }
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) acc = dot_chunk(xv[i], g0v[i], g1v[i], gmv[i], acc);
+  } else {
+    for (int c = lane; c < nc; c += 64) acc = dot_chunk(xr[c], gr[2 * c], gr[2 * c + 1], gamma_chunk(gamma, c), acc);
   }
   const float s = wave_sum(acc);
   const float r = rstd[t];
   const float c2 = ((r * r) * r) * s / (float)d;
   float4* out = dx + t * (int64_t)(d / 4);
-  for (int c = lane; c < nc; c += 64) {
-    const uint4 v = xr[c];
-    const float4 g0 = gr[2 * c], g1 = gr[2 * c + 1];
+  // dx = r g G - c2 x over chunk c
+  auto out_chunk = [&](int c, uint4 v, float4 g0, float4 g1, uint4 gv) {
     const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
     const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    uint32_t gm[4] = {0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
-    if (gamma) {
-      const uint4 gv = gamma[c];
-      gm[0] = gv.x, gm[1] = gv.y, gm[2] = gv.z, gm[3] = gv.w;
-    }
+    const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
     float o[8];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -131,6 +168,12 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x
     }
     out[2 * c] = float4{o[0], o[1], o[2], o[3]};
     out[2 * c + 1] = float4{o[4], o[5], o[6], o[7]};
+  };
+  if constexpr (NCL > 0) {
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) out_chunk(lane + 64 * i, xv[i], g0v[i], g1v[i], gmv[i]);
+  } else {
+    for (int c = lane; c < nc; c += 64) out_chunk(c, xr[c], gr[2 * c], gr[2 * c + 1], gamma_chunk(gamma, c));
   }
 }
 
@@ -168,8 +211,16 @@ hipError_t launch_rmsnorm(const void* x, const void* gamma, int64_t T, int d, fl
   if (T <= 0) return hipSuccess;
   const int64_t nb = (T + 3) / 4;
   if (nb > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(rmsnorm_fwd, dim3((unsigned)nb), dim3(256), 0, s, (const uint4*)x, (const uint4*)gamma, T, d,
-                     eps, (uint4*)h, rstd);
+  const dim3 g((unsigned)nb), b(256);
+  const uint4* xp = (const uint4*)x;
+  const uint4* gp = (const uint4*)gamma;
+  switch (d) {  // widths whose rows stay in registers
+    case 2048: hipLaunchKernelGGL(rmsnorm_fwd<4>, g, b, 0, s, xp, gp, T, d, eps, (uint4*)h, rstd); break;
+    case 4096: hipLaunchKernelGGL(rmsnorm_fwd<8>, g, b, 0, s, xp, gp, T, d, eps, (uint4*)h, rstd); break;
+    case 5120: hipLaunchKernelGGL(rmsnorm_fwd<10>, g, b, 0, s, xp, gp, T, d, eps, (uint4*)h, rstd); break;
+    case 8192: hipLaunchKernelGGL(rmsnorm_fwd<16>, g, b, 0, s, xp, gp, T, d, eps, (uint4*)h, rstd); break;
+    default: hipLaunchKernelGGL(rmsnorm_fwd<0>, g, b, 0, s, xp, gp, T, d, eps, (uint4*)h, rstd); break;
+  }
   return hipGetLastError();
 }
 
@@ -179,8 +230,16 @@ hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float
   if (T > 0 && grad_x) {
     const int64_t nb = (T + 3) / 4;
     if (nb > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(rmsnorm_bwd_x, dim3((unsigned)nb), dim3(256), 0, s, (const uint4*)x, (const uint4*)gamma,
-                       rstd, (const float4*)grad_h, T, d, (float4*)grad_x);
+    const dim3 g((unsigned)nb), b(256);
+    const uint4* xp = (const uint4*)x;
+    const uint4* gp = (const uint4*)gamma;
+    const float4* Gp = (const float4*)grad_h;
+    switch (d) {  // widths whose rows stay in registers
+      case 2048: hipLaunchKernelGGL(rmsnorm_bwd_x<4>, g, b, 0, s, xp, gp, rstd, Gp, T, d, (float4*)grad_x); break;
+      case 4096: hipLaunchKernelGGL(rmsnorm_bwd_x<8>, g, b, 0, s, xp, gp, rstd, Gp, T, d, (float4*)grad_x); break;
+      case 5120: hipLaunchKernelGGL(rmsnorm_bwd_x<10>, g, b, 0, s, xp, gp, rstd, Gp, T, d, (float4*)grad_x); break;
+      default: hipLaunchKernelGGL(rmsnorm_bwd_x<0>, g, b, 0, s, xp, gp, rstd, Gp, T, d, (float4*)grad_x); break;
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
