@@ -14,7 +14,11 @@
 // Backward, with G = dL/dh (fp32) and the casts passed straight through:
 //   dx_k = r g_k G_k - (r^3 s / d) x_k,   s = sum_j G_j g_j x_j   (one wavefront per row)
 //   dg_k = sum_t G_tk x_tk r_t   as fixed-order column sums over blocks of 256
-//          rows, then over the blocks in order (no atomics).
+//          rows, then over the blocks in order (no atomics). Within a block the
+//          rows go in order, except in calls of at least 65536 rows of width
+//          2048 or 4096, whose grad_x pass also forms the block sums: there each
+//          quarter of 64 rows goes in order and the quarters combine as
+//          (q0 + q1) + (q2 + q3).
 // Each is one HBM pass over the rows; the norm costs ~0.2% of the LM head it
 // feeds, so it runs as its own launch ahead of the head instead of inside the
 // head's MFMA loop, which would repeat it once per vocabulary tile and add
@@ -110,6 +114,35 @@ __device__ __forceinline__ uint4 gamma_chunk(const uint4* __restrict__ gamma, in
   return gamma ? gamma[c] : uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u};
 }
 
+// s += G g x over one chunk, in element order
+__device__ __forceinline__ float dot_chunk(uint4 v, float4 g0, float4 g1, uint4 gv, float acc) {
+  const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc = __builtin_fmaf(gg[2 * i] * bf16_lo(gm[i]), bf16_lo(w[i]), acc);
+    acc = __builtin_fmaf(gg[2 * i + 1] * bf16_hi(gm[i]), bf16_hi(w[i]), acc);
+  }
+  return acc;
+}
+
+// dx = r g G - c2 x over chunk c of a row
+__device__ __forceinline__ void out_chunk_dx(float4* __restrict__ out, int c, uint4 v, float4 g0, float4 g1, uint4 gv,
+                                             float r, float c2) {
+  const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+  const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
+  float o[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = r * (bf16_lo(gm[i]) * gg[2 * i]) - c2 * bf16_lo(w[i]);
+    o[2 * i + 1] = r * (bf16_hi(gm[i]) * gg[2 * i + 1]) - c2 * bf16_hi(w[i]);
+  }
+  out[2 * c] = float4{o[0], o[1], o[2], o[3]};
+  out[2 * c + 1] = float4{o[4], o[5], o[6], o[7]};
+}
+
 // Same two-mode structure as the forward (NCL > 0: the row's x, G and gamma
 // chunks kept in registers between the passes).
 template <int NCL>
@@ -122,18 +155,6 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x
   const int nc = NCL > 0 ? NCL * 64 : d / 8;
   const uint4* xr = x + t * nc;
   const float4* gr = G + t * (int64_t)(d / 4);
-  // s += G g x over chunk c, in element order
-  auto dot_chunk = [](uint4 v, float4 g0, float4 g1, uint4 gv, float acc) {
-    const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      acc = __builtin_fmaf(gg[2 * i] * bf16_lo(gm[i]), bf16_lo(w[i]), acc);
-      acc = __builtin_fmaf(gg[2 * i + 1] * bf16_hi(gm[i]), bf16_hi(w[i]), acc);
-    }
-    return acc;
-  };
   uint4 xv[NCL > 0 ? NCL : 1], gmv[NCL > 0 ? NCL : 1];
   float4 g0v[NCL > 0 ? NCL : 1], g1v[NCL > 0 ? NCL : 1];
   float acc = 0.f;
@@ -155,25 +176,83 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x
   const float r = rstd[t];
   const float c2 = ((r * r) * r) * s / (float)d;
   float4* out = dx + t * (int64_t)(d / 4);
-  // dx = r g G - c2 x over chunk c
-  auto out_chunk = [&](int c, uint4 v, float4 g0, float4 g1, uint4 gv) {
-    const float gg[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-    const uint32_t gm[4] = {gv.x, gv.y, gv.z, gv.w};
-    float o[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      o[2 * i] = r * (bf16_lo(gm[i]) * gg[2 * i]) - c2 * bf16_lo(w[i]);
-      o[2 * i + 1] = r * (bf16_hi(gm[i]) * gg[2 * i + 1]) - c2 * bf16_hi(w[i]);
-    }
-    out[2 * c] = float4{o[0], o[1], o[2], o[3]};
-    out[2 * c + 1] = float4{o[4], o[5], o[6], o[7]};
-  };
   if constexpr (NCL > 0) {
 #pragma unroll
-    for (int i = 0; i < NCL; ++i) out_chunk(lane + 64 * i, xv[i], g0v[i], g1v[i], gmv[i]);
+    for (int i = 0; i < NCL; ++i) out_chunk_dx(out, lane + 64 * i, xv[i], g0v[i], g1v[i], gmv[i], r, c2);
   } else {
-    for (int c = lane; c < nc; c += 64) out_chunk(c, xr[c], gr[2 * c], gr[2 * c + 1], gamma_chunk(gamma, c));
+    for (int c = lane; c < nc; c += 64)
+      out_chunk_dx(out, c, xr[c], gr[2 * c], gr[2 * c + 1], gamma_chunk(gamma, c), r, c2);
+  }
+}
+
+// Widths whose rows stay in registers: grad_x and the block's grad_gamma
+// column sums in one pass over x and G. One workgroup per block of 256 rows;
+// wave w takes the block's rows 64 w .. 64 w + 63 in order, each as
+// rmsnorm_bwd_x does (the same dx), and adds (G x) r of its columns to its own
+// column sums in LDS in that row order; the four waves' sums then combine as
+// (q0 + q1) + (q2 + q3) into the block's partial. The sums over the blocks in
+// order follow in rmsnorm_dgamma_final.
+template <int NCL, bool WANT_X>
+__global__ __launch_bounds__(256) void rmsnorm_bwd_fused(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
+                                                         const float* __restrict__ rstd, const float4* __restrict__ G,
+                                                         int64_t T, float4* __restrict__ dx, float* __restrict__ part) {
+  constexpr int d = NCL * 512, nc = NCL * 64;
+  __shared__ float4 red[4][nc][2];  // each wave's column sums, 8 per chunk
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t b0 = (int64_t)blockIdx.x * 256;
+#pragma unroll
+  for (int i = 0; i < NCL; ++i) red[wave][lane + 64 * i][0] = red[wave][lane + 64 * i][1] = float4{0.f, 0.f, 0.f, 0.f};
+  const int64_t r_end = (T - b0) < 256 ? T - b0 : 256;
+#pragma unroll 1
+  for (int j = 0; j < 64; ++j) {
+    const int64_t rl = 64 * wave + j;
+    if (rl >= r_end) break;  // uniform across the wave
+    const int64_t t = b0 + rl;
+    const uint4* xr = x + t * nc;
+    const float4* gr = G + t * (int64_t)(d / 4);
+    uint4 xv[NCL], gmv[NCL];
+    float4 g0v[NCL], g1v[NCL];
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) {
+      const int c = lane + 64 * i;
+      xv[i] = xr[c];
+      g0v[i] = gr[2 * c];
+      g1v[i] = gr[2 * c + 1];
+      gmv[i] = gamma_chunk(gamma, c);
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) acc = dot_chunk(xv[i], g0v[i], g1v[i], gmv[i], acc);
+    const float sdot = wave_sum(acc);
+    const float r = rstd[t];
+    const float c2 = ((r * r) * r) * sdot / (float)d;
+    float4* out = dx + t * (int64_t)(d / 4);
+    // per chunk: its dx (WANT_X), then its (G x) r added to the column sums
+#pragma unroll
+    for (int i = 0; i < NCL; ++i) {
+      const int c = lane + 64 * i;
+      if constexpr (WANT_X) out_chunk_dx(out, c, xv[i], g0v[i], g1v[i], gmv[i], r, c2);
+      const uint32_t w[4] = {xv[i].x, xv[i].y, xv[i].z, xv[i].w};
+      const float gg[8] = {g0v[i].x, g0v[i].y, g0v[i].z, g0v[i].w, g1v[i].x, g1v[i].y, g1v[i].z, g1v[i].w};
+      float e[8];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        e[2 * k] = (gg[2 * k] * bf16_lo(w[k])) * r;
+        e[2 * k + 1] = (gg[2 * k + 1] * bf16_hi(w[k])) * r;
+      }
+      const float4 p0 = red[wave][c][0], p1 = red[wave][c][1];
+      red[wave][c][0] = float4{p0.x + e[0], p0.y + e[1], p0.z + e[2], p0.w + e[3]};
+      red[wave][c][1] = float4{p1.x + e[4], p1.y + e[5], p1.z + e[6], p1.w + e[7]};
+    }
+  }
+  __syncthreads();
+  // (q0 + q1) + (q2 + q3), the block's 8 NCL columns per lane spread over the four waves
+  auto add4 = [](float4 a, float4 b) { return float4{a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w}; };
+  float4* po = (float4*)(part + (int64_t)blockIdx.x * d);
+  for (int c = threadIdx.x; c < nc; c += 256) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+      po[2 * c + hh] = add4(add4(red[0][c][hh], red[1][c][hh]), add4(red[2][c][hh], red[3][c][hh]));
   }
 }
 
@@ -224,10 +303,37 @@ hipError_t launch_rmsnorm(const void* x, const void* gamma, int64_t T, int d, fl
   return hipGetLastError();
 }
 
+// Rows from which the norm backward takes grad_gamma in the grad_x pass.
+constexpr int64_t kFusedNormRows = 65536;
+
+template <int NCL>
+static hipError_t launch_fused(const void* x, const void* gamma, const float* rstd, const float* grad_h, int64_t T,
+                               float* grad_x, float* part, hipStream_t s) {
+  const dim3 g((unsigned)((T + 255) / 256)), b(256);
+  if (grad_x)
+    hipLaunchKernelGGL((rmsnorm_bwd_fused<NCL, true>), g, b, 0, s, (const uint4*)x, (const uint4*)gamma, rstd,
+                       (const float4*)grad_h, T, (float4*)grad_x, part);
+  else
+    hipLaunchKernelGGL((rmsnorm_bwd_fused<NCL, false>), g, b, 0, s, (const uint4*)x, (const uint4*)gamma, rstd,
+                       (const float4*)grad_h, T, (float4*)nullptr, part);
+  return hipGetLastError();
+}
+
 hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float* rstd, const float* grad_h,
                                    int64_t T, int d, float* grad_x, float* grad_gamma, int accumulate, float* part,
                                    hipStream_t s) {
-  if (T > 0 && grad_x) {
+  // Large calls at the widths whose rows stay in registers take grad_gamma's
+  // block sums in the grad_x pass (with or without grad_x): one workgroup per
+  // 256 rows walks its rows in order, which pays once there are enough blocks
+  // to fill the chip. The choice depends on (T, d) only.
+  const bool fused = grad_gamma && (d == 2048 || d == 4096) && T >= kFusedNormRows;
+  if (fused && T > 0) {
+    if ((T + 255) / 256 > 65535) return hipErrorInvalidValue;
+    const hipError_t e = d == 2048 ? launch_fused<4>(x, gamma, rstd, grad_h, T, grad_x, part, s)
+                                   : launch_fused<8>(x, gamma, rstd, grad_h, T, grad_x, part, s);
+    if (e != hipSuccess) return e;
+  }
+  if (T > 0 && grad_x && !fused) {
     const int64_t nb = (T + 3) / 4;
     if (nb > 0x7fffffff) return hipErrorInvalidValue;
     const dim3 g((unsigned)nb), b(256);
@@ -247,7 +353,7 @@ hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float
     const int64_t n_blocks = (T + 255) / 256;
     if (n_blocks > 65535) return hipErrorInvalidValue;
     const unsigned gx = (unsigned)((d + 255) / 256);
-    if (n_blocks > 0) {
+    if (n_blocks > 0 && !fused) {
       hipLaunchKernelGGL(rmsnorm_dgamma_part, dim3(gx, (unsigned)n_blocks), dim3(256), 0, s, (const uint16_t*)x, rstd,
                          grad_h, T, d, part);
       const hipError_t e = hipGetLastError();

@@ -167,3 +167,40 @@ def test_rmsnorm_degenerate_calls():
     assert (buf == 5.0).all()
     h, r = tim.rmsnorm(e)
     assert h.shape == (0, d) and r.shape == (0,)
+
+
+@pytest.mark.parametrize("d,with_gamma", [(2048, True), (4096, False)])
+def test_rmsnorm_backward_large_call_vs_oracle(d, with_gamma):
+    """Calls of at least 65536 rows at d = 2048 / 4096 form grad_gamma's block
+    sums in the grad_x pass (64-row quarters, then (q0 + q1) + (q2 + q3)):
+    grad_gamma against the oracle within its bound, grad_x bitwise equal to the
+    same rows evaluated alone (the smaller call's path) and to the oracle on
+    sampled rows, and grad_gamma without grad_x the same bits."""
+    T = 65536 + 77
+    print(f"case large T={T} d={d} gamma={with_gamma}", flush=True)
+    x = _x(T, d, d + 7)
+    g = _gamma(d, d + 8) if with_gamma else None
+    eps = 1e-6
+    _, rstd = tim.rmsnorm(x, g, eps)
+    G = torch.randn(T, d, generator=torch.Generator(device="cuda").manual_seed(d), device="cuda")
+    gx, gg = tim.rmsnorm_backward(x, g, rstd, G)
+    _, gg_only = tim.rmsnorm_backward(x, g, rstd, G, want_x=False)
+    torch.cuda.synchronize()
+    assert bits_equal(gg_only, gg)
+    rows = [0, 1, 255, 256, 4097, 65535, T - 1]
+    for r in rows:
+        gx1, _ = tim.rmsnorm_backward(x[r:r + 1].contiguous(), g, rstd[r:r + 1].contiguous(), G[r:r + 1].contiguous(),
+                                      want_gamma=False)
+        assert bits_equal(gx1, gx[r:r + 1].contiguous())
+    gb = None if g is None else bf16_bits(g)
+    Gn = G.double().cpu().numpy()
+    xb = bf16_bits(x)
+    dx, dg = oracle.rmsnorm_grads(xb, gb, eps, Gn)
+    xf = oracle.bf16_to_f64(xb)
+    r_ = 1.0 / np.sqrt((xf * xf).mean(axis=1) + eps)
+    mag_g = np.abs(Gn * xf * r_[:, None]).sum(axis=0)
+    err_g = np.abs(gg.double().cpu().numpy() - dg)
+    rg = (err_g / ((256 + T / 256 + 32) * U * mag_g + 1e-30)).max()
+    err_x = np.abs(gx.double().cpu().numpy()[rows] - dx[rows]).max() / np.abs(dx[rows]).max()
+    print(f"[parity] large rmsnorm backward d={d}: grad_gamma max err/bound {rg:.3f}, grad_x max rel err {err_x:.2e}")
+    assert rg <= 1.0 and err_x <= 1e-5
