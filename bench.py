@@ -404,7 +404,7 @@ def main(argv=None):
         norm_sample = (idx_n, bf16_bits(h.index_select(0, it_n)), bf16_bits(gam), G_n.index_select(0, it_n).double().cpu().numpy(),
                        bf16_bits(h_n.index_select(0, it_n)), gx_n.index_select(0, it_n).double().cpu().numpy())
     nf_bytes = 4.0 * T * d + 4.0 * T
-    nb_bytes = 16.0 * T * d
+    nb_bytes = 10.0 * T * d + 4.0 * T  # x (2 B) and G (4 B) read, grad_x (4 B) written per element; rstd
     norm = {"forward_ms": nf_ms, "forward_GBps": nf_bytes / (nf_ms / 1e3) / 1e9,
             "forward_frac": nf_bytes / (nf_ms / 1e3) / 1e9 / PEAK_HBM_GBS, "forward_bytes": nf_bytes,
             "backward_ms": nb_ms, "backward_GBps": nb_bytes / (nb_ms / 1e3) / 1e9,
