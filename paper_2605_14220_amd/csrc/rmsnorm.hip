@@ -279,7 +279,16 @@ __global__ __launch_bounds__(256) void rmsnorm_dgamma_final(const float* __restr
   const int k = blockIdx.x * 256 + threadIdx.x;
   if (k >= d) return;
   float acc = accumulate ? dg[k] : 0.f;
-  for (int b = 0; b < n_blocks; ++b) acc = acc + part[(int64_t)b * d + k];
+  int b = 0;
+  // 16 loads issued ahead of their adds (the adds stay in block order)
+  for (; b + 16 <= n_blocks; b += 16) {
+    float v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) v[i] = part[(int64_t)(b + i) * d + k];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc = acc + v[i];
+  }
+  for (; b < n_blocks; ++b) acc = acc + part[(int64_t)b * d + k];
   dg[k] = acc;
 }
 
