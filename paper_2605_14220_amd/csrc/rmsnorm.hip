@@ -266,7 +266,20 @@ __global__ __launch_bounds__(256) void rmsnorm_dgamma_part(const uint16_t* __res
   const int64_t t0 = (int64_t)blockIdx.y * 256;
   const int64_t t1 = (T - t0) < 256 ? T : t0 + 256;
   float acc = 0.f;
-  for (int64_t t = t0; t < t1; ++t) {
+  int64_t t = t0;
+  // 8 rows' loads issued ahead of their terms (the adds stay in row order)
+  for (; t + 8 <= t1; t += 8) {
+    float xv[8], gv[8], rv[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      xv[i] = __uint_as_float((uint32_t)x[(t + i) * d + k] << 16);
+      gv[i] = G[(t + i) * d + k];
+      rv[i] = rstd[t + i];
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc = acc + (gv[i] * xv[i]) * rv[i];
+  }
+  for (; t < t1; ++t) {
     const float xv = __uint_as_float((uint32_t)x[t * d + k] << 16);
     acc = acc + (G[t * d + k] * xv) * rstd[t];
   }
