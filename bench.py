@@ -199,8 +199,8 @@ def main(argv=None):
                     help="skip the backward measurement")
     args = ap.parse_args(argv)
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this path runs on a single GPU, "
-              f"see the sharding notes in DESIGN.md)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: this path runs on a single GPU "
+              f"(token- or vocabulary-parallel sharding is a design note only, not built)", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
