@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_fused(const uint4* __restrict
     const float sdot = wave_sum(acc);
     const float r = rstd[t];
     const float c2 = ((r * r) * r) * sdot / (float)d;
-    float4* out = dx + t * (int64_t)(d / 4);
+    float4* out = WANT_X ? dx + t * (int64_t)(d / 4) : nullptr;
     // per chunk: its dx (WANT_X), then its (G x) r added to the column sums
 #pragma unroll
     for (int i = 0; i < NCL; ++i) {
