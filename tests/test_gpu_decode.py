@@ -3,10 +3,10 @@
 Decode batches (rollout mode) take half vocabulary tiles -- one vocab wave
 per workgroup, a partial per 128-entry half of each tile, the two halves
 merged (lower first) in the merge pass -- always for 65..128 rows (two
-workgroups per CU against one), and for at most 64 rows where they fill the
-chip's rounds more evenly than whole tiles (V = 151936 on 256 CUs: 1187 halves
-on 768 slots against 594 tiles on 512). Launches of at most 512 rows merge
-with four waves per row. The tests cover vocabulary sizes whose last tile is
+workgroups per CU against one), and up to 64 rows where they fill the chip's
+rounds more evenly than whole tiles (V = 151936 on 256 CUs: 1187 halves on
+768 slots against 594 tiles on 512). Launches of at most 512 rows merge with
+four waves per row. The tests cover vocabulary sizes whose last tile is
 whole, has a partial upper half, only a lower half, or a partial lower half,
 tokens in every lane-group position of both halves and in the last tile, and
 the fp64 oracle."""
@@ -48,14 +48,19 @@ def _fill(units, slots):
     return units / (-(-units // slots) * slots)
 
 
-def _takes_halves(V, T):
-    """The planner's choice on this device: always above 64 rows; up to 64,
-    half tiles (3 workgroups per CU) when their last round leaves fewer slots
-    idle than whole tiles (2 per CU)."""
+def _per_row(V, T):
+    """Partials per row of the planner's choice on this device: halves above
+    64 rows; up to 64, half tiles (3 workgroups per CU) when their last round
+    leaves fewer slots idle than whole tiles (2 per CU), else whole tiles."""
+    nv, nh = -(-V // 256), -(-V // 128)
     if T > 64:
-        return True
+        return nh
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    return _fill(-(-V // 128), 3 * cus) > _fill(-(-V // 256), 2 * cus)
+    return nh if _fill(nh, 3 * cus) > _fill(nv, 2 * cus) else nv
+
+
+def _shape(V, T):
+    return "half" if _per_row(V, T) == -(-V // 128) else "whole"
 
 
 def _decode(h, W, tok, tau):
@@ -74,7 +79,7 @@ def _decode(h, W, tok, tau):
 
 
 @pytest.mark.parametrize("V", [1, 2, 127, 128, 129, 255, 256, 257, 383, 384, 385, 4096 + 77, 4096 + 200,
-                               151936, 152064])
+                               151936, 152064, 512 * 256 + 77, 512 * 256 + 200, 600 * 256])
 @pytest.mark.parametrize("T", [1, 19, 64, 65, 100, 128])
 def test_decode_bitwise_equal_whole_tiles(V, T):
     d = 256
@@ -82,8 +87,8 @@ def test_decode_bitwise_equal_whole_tiles(V, T):
     h, W = inputs(T, d, V, seed=V % 1000 + T, w_std=0.1)
     tok = _tokens(T, V, seed=V + T)
     dec, per_row = _decode(h, W, tok, 0.7)
-    assert per_row == (-(-V // 128) if _takes_halves(V, T) else -(-V // 256))
-    print(f"  {'half' if _takes_halves(V, T) else 'whole'} tiles, {per_row} partials per row", flush=True)
+    assert per_row == _per_row(V, T)
+    print(f"  {_shape(V, T)} tiles, {per_row} partials per row", flush=True)
     trn = tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, lse=True)        # whole tiles
     _same(dec, trn)
     if V <= 4096 + 200:
@@ -100,7 +105,9 @@ def test_halves_full_size_rows_against_oracle():
     tok = _tokens(T, V, seed=41)
     dec, per_row = _decode(h, W, tok, 1.0)
     if torch.cuda.get_device_properties(0).multi_processor_count == 256:
-        assert _takes_halves(V, T) and per_row == 1187      # 1187 halves on 768 slots beat 594 tiles on 512
+        assert per_row == 1187      # 1187 halves on 768 slots beat 594 tiles on 512
+    else:
+        assert per_row == _per_row(V, T)
     trn = tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING, lse=True)
     _same(dec, trn)
     ref_lp, ref_H = oracle_rows(h, W, tok, 1.0)
@@ -116,7 +123,7 @@ def test_halves_gather_is_bit_exact():
     for base in (256, 384):
         tok = (torch.arange(T, dtype=torch.int32) * 2 + base + (1 if base == 384 else 0)).cuda()
         (lp, _, lse), per_row = _decode(h, W, tok, 0.8)
-        assert per_row == (8 if _takes_halves(V, T) else 4)
+        assert per_row == _per_row(V, T)
         z = tim.logits(h, W, 0.8)
         ztok = z.gather(1, tok.long()[:, None])[:, 0]
         assert bits_equal(lp, ztok - lse)
@@ -188,7 +195,7 @@ def test_decode_128_row_tiles_full_size():
     trn = tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING, lse=True)
     for n in (65, 100, 128):
         dec, per_row = _decode(h[:n].contiguous(), W, tok[:n].contiguous(), 1.0)
-        assert per_row == 1187
+        assert per_row == _per_row(V, n)
         for x, y in zip(dec, trn):
             assert bits_equal(x, y[:n])
     rows = [0, 1, 63, 64, 65, 99, 127]
