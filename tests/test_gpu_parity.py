@@ -179,3 +179,24 @@ def test_duplicated_vocabulary_shifts_by_log2(V, mode):
     lp2, H2, _ = tim.logprobs(h, W2, tok, 1.0, mode=mode)
     check_close(f"dup logp V={V}", lp2, (lp.double() - math.log(2)).cpu().numpy(), 5e-6)
     check_close(f"dup entropy V={V}", H2, (H.double() + math.log(2)).cpu().numpy(), 2e-5)
+
+
+@pytest.mark.parametrize("mode", [Mode.TRAINING, Mode.ROLLOUT])
+def test_non_finite_rows_stay_in_their_rows(mode):
+    """A NaN or Inf in a row's hidden state gives that row non-finite outputs;
+    every other row of the launch is bitwise what it is without them (no
+    reduction crosses rows)."""
+    T, d, V = 64, 256, 3000
+    h, W = inputs(T, d, V, seed=48)
+    tok = random_tokens(T, V, seed=48)
+    clean = tim.logprobs(h, W, tok, 1.0, mode=mode, lse=True)
+    bad = h.clone()
+    bad[3, 17] = float("nan")
+    bad[40, 0] = float("inf")
+    bad[41, :] = float("nan")
+    out = tim.logprobs(bad, W, tok, 1.0, mode=mode, lse=True)
+    for r in (3, 40, 41):
+        assert not torch.isfinite(out[0][r]) and not torch.isfinite(out[1][r])
+    ok = [i for i in range(T) if i not in (3, 40, 41)]
+    for x, y in zip(out, clean):
+        assert bits_equal(x[ok], y[ok])
