@@ -200,3 +200,21 @@ def test_non_finite_rows_stay_in_their_rows(mode):
     ok = [i for i in range(T) if i not in (3, 40, 41)]
     for x, y in zip(out, clean):
         assert bits_equal(x[ok], y[ok])
+
+
+@pytest.mark.parametrize("T,d,V,tau,w_std,mode", [
+    (40, 256, 5000, 0.02, 0.1, Mode.TRAINING),    # logits spread over hundreds of nats: most exps underflow
+    (40, 256, 5000, 50.0, 0.1, Mode.ROLLOUT),     # near-uniform rows
+    (70, 8192, 1000, 1.0, None, Mode.TRAINING),   # twice the headline's hidden size (128 stages per tile)
+])
+def test_extreme_temperatures_and_wide_rows(T, d, V, tau, w_std, mode):
+    print(f"case T={T} d={d} V={V} tau={tau} {mode.name}", flush=True)
+    h, W = inputs(T, d, V, seed=49 + d, w_std=w_std)
+    tok = random_tokens(T, V, seed=49)
+    lp, H, _ = tim.logprobs(h, W, tok, tau, mode=mode, lse=True)
+    ref_lp, ref_H = oracle_rows(h, W, tok, tau)
+    check_close(f"logp tau={tau} d={d}", lp, ref_lp, TOL_LOGP)
+    check_close(f"entropy tau={tau} d={d}", H, ref_H, TOL_ENT)
+    other = Mode.ROLLOUT if mode == Mode.TRAINING else Mode.TRAINING
+    for x, y in zip(tim.logprobs(h, W, tok, tau, mode=other, lse=True), (lp, H)):
+        assert bits_equal(x, y)
