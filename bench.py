@@ -70,8 +70,9 @@ def load_traffic(name: str):
         return None
 
 
-def cpu_baseline(h, W, tok, tau, rows: int, seed: int = 7):
-    """Time the fp64 oracle on a seeded sample of rows on the host cores."""
+def cpu_baseline(h, W, tok, tau, rows: int, seed: int = 7, threads: int | None = None):
+    """Time the fp64 oracle on a seeded sample of rows on the host cores (all
+    of them, or `threads`)."""
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
@@ -85,11 +86,13 @@ def cpu_baseline(h, W, tok, tau, rows: int, seed: int = 7):
     hb = bf16_bits(h.index_select(0, it))
     tb = tok.index_select(0, it).cpu().numpy()
     wb = bf16_bits(W)
-    t0 = time.perf_counter()
-    lp, ent = oracle.logprobs(hb, wb, tb, tau)
-    dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return idx, lp, ent, dt, threads
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=threads):
+        t0 = time.perf_counter()
+        lp, ent = oracle.logprobs(hb, wb, tb, tau)
+        dt = time.perf_counter() - t0
+        used = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return idx, lp, ent, dt, used
 
 
 def _threads():
@@ -466,6 +469,7 @@ def main(argv=None):
            "C": 2.0}
 
     cpu = None
+    cpu_single = None
     parity = None
     mstats = None
     if args.cpu_rows > 0:
@@ -480,6 +484,11 @@ def main(argv=None):
         parity = {"rows": int(args.cpu_rows), "max_abs_dlogp": e_lp, "max_abs_dentropy": e_h}
         log(f"[bench] oracle: {cpu['value']:.1f} tokens/s on {threads} threads; parity on sample: "
             f"max|dlogp|={e_lp:.2e} max|dH|={e_h:.2e}")
+        n1 = max(1, args.cpu_rows // 16)
+        _, _, _, dt1, thr1 = cpu_baseline(h, W, tok, tau, n1, seed=8, threads=1)
+        cpu_single = {"value": n1 / dt1, "unit": "tokens/s", "cores": int(thr1), "kind": "oracle",
+                      "sample": f"{n1} seeded rows (seed 8) of the {T}-token stream, one thread, {dt1:.1f} s"}
+        log(f"[bench] oracle on one thread: {cpu_single['value']:.1f} tokens/s ({n1} rows)")
         log("[bench] oracle beside the other rows ...")
         beside = oracle_beside(dev, T, tau, cu, adv, norm_sample, bwd_sample, W)
         for key, obj in (("mismatch", None), ("seq", seq), ("ppo", ppo), ("rmsnorm", norm), ("backward", bwd)):
@@ -512,6 +521,7 @@ def main(argv=None):
                      "traffic": traffic,
                      "kernel": "lmhead_partials", "launch_ms": avg_ms, "flop_per_launch": flop_per_launch},
         "cpu_baseline": cpu,
+        "cpu_baseline_single_thread": cpu_single,
         "parity_sample": parity,
         "mismatch_vs_splitk4": mis,
         "mismatch_stats": mstats,
