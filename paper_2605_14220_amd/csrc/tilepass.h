@@ -20,6 +20,8 @@
 // finished tile (softmax partials, logit gradients, plain fp32 stores).
 #pragma once
 
+#include <atomic>
+
 #include "kernels.h"
 
 namespace tim {
@@ -571,11 +573,16 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
 static int device_cu_count() {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
-  static int cache[64] = {0};
-  if (dev < 64 && cache[dev] > 0) return cache[dev];
+  // atomic: host threads may launch on one device at once (a racing first
+  // call only queries the same attribute twice)
+  static std::atomic<int> cache[64];
+  if (dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
   int n = 0;
   if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (dev < 64) cache[dev] = n;
+  if (dev < 64) cache[dev].store(n, std::memory_order_relaxed);
   return n;
 }
 
