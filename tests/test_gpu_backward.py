@@ -111,6 +111,7 @@ def test_logit_grads_vs_oracle(T, d, V, tau, entropy):
     (700, 640, 5000, 0.5, 256, True),
     (130, 128, 777, 2.0, 0, False),
     (1, 128, 300, 1.0, 0, True),
+    (200, 8192, 1000, 0.3, 128, True),   # a long hidden chain, a sharp distribution
 ])
 def test_backward_vs_oracle(T, d, V, tau, mb, entropy):
     print(f"case T={T} d={d} V={V} tau={tau} mb={mb} entropy={entropy}", flush=True)

@@ -120,7 +120,7 @@ def test_norm_feeds_the_lm_head():
 
 # 2048, 4096 and 5120 keep the row in registers between the passes; the others reread it
 @pytest.mark.parametrize("T,d,with_gamma", [(300, 640, True), (513, 256, False), (1, 8, True), (257, 2048, True),
-                                            (130, 4096, False), (66, 5120, True)])
+                                            (130, 4096, False), (66, 5120, True), (40, 8192, True)])
 def test_rmsnorm_backward_vs_oracle(T, d, with_gamma):
     print(f"case T={T} d={d} gamma={with_gamma}", flush=True)
     x = _x(T, d, 3 * T + d)
