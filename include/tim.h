@@ -307,9 +307,10 @@ tim_status tim_rmsnorm(const void* x, const void* gamma, int64_t T, int32_t d, f
  *   grad_gamma[k] (+)= sum_t G_tk x_tk rstd_t                                (fp32 [d])
  * (g = gamma, or ones when NULL). grad_x's row sum runs in the forward's
  * fixed order (batch-invariant); grad_gamma sums blocks of 256 rows in row
- * order (for T >= 65536 and d = 2048 or 4096: each 64-row quarter of a block
- * in row order, the quarters as (q0 + q1) + (q2 + q3)), then the blocks in
- * order: deterministic, no atomics. Either output may
+ * order (for T >= 65536 and d = 2048 or 4096: blocks of 4 q rows, q = max(64,
+ * ceil(T / (4 n))) with n = 512 at d = 4096 and 1024 at d = 2048, each q-row
+ * quarter of a block in row order, the quarters as (q0 + q1) + (q2 + q3)),
+ * then the blocks in order: deterministic, no atomics. Either output may
  * be NULL (not computed); with accumulate_grad_gamma = 1 the result is added
  * to grad_gamma's contents. The workspace holds
  * tim_rmsnorm_backward_workspace_size(T, d) = ceil(T / 256) * d * 4 bytes

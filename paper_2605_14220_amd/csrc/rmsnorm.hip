@@ -25,6 +25,7 @@
 // VALU work to the loop that bounds the head.
 
 #include <hip/hip_runtime.h>
+#include <algorithm>
 
 #include "kernels.h"
 
@@ -186,8 +187,8 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x
 }
 
 // Widths whose rows stay in registers: grad_x and the block's grad_gamma
-// column sums in one pass over x and G. One workgroup per block of 256 rows;
-// wave w takes the block's rows 64 w .. 64 w + 63 in order, each as
+// column sums in one pass over x and G. One workgroup per block of 4 rpw rows;
+// wave w takes the block's rows rpw w .. rpw w + rpw - 1 in order, each as
 // rmsnorm_bwd_x does (the same dx), and adds (G x) r of its columns to its own
 // column sums in LDS in that row order; the four waves' sums then combine as
 // (q0 + q1) + (q2 + q3) into the block's partial. The sums over the blocks in
@@ -195,17 +196,18 @@ __global__ __launch_bounds__(256) void rmsnorm_bwd_x(const uint4* __restrict__ x
 template <int NCL, bool WANT_X>
 __global__ __launch_bounds__(256) void rmsnorm_bwd_fused(const uint4* __restrict__ x, const uint4* __restrict__ gamma,
                                                          const float* __restrict__ rstd, const float4* __restrict__ G,
-                                                         int64_t T, float4* __restrict__ dx, float* __restrict__ part) {
+                                                         int64_t T, int rpw, float4* __restrict__ dx,
+                                                         float* __restrict__ part) {
   constexpr int d = NCL * 512, nc = NCL * 64;
   __shared__ float4 red[4][nc][2];  // each wave's column sums, 8 per chunk
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t b0 = (int64_t)blockIdx.x * 256;
+  const int64_t b0 = (int64_t)blockIdx.x * 4 * rpw;
 #pragma unroll
   for (int i = 0; i < NCL; ++i) red[wave][lane + 64 * i][0] = red[wave][lane + 64 * i][1] = float4{0.f, 0.f, 0.f, 0.f};
-  const int64_t r_end = (T - b0) < 256 ? T - b0 : 256;
+  const int64_t r_end = (T - b0) < 4 * rpw ? T - b0 : 4 * rpw;
 #pragma unroll 1
-  for (int j = 0; j < 64; ++j) {
-    const int64_t rl = 64 * wave + j;
+  for (int j = 0; j < rpw; ++j) {
+    const int64_t rl = (int64_t)rpw * wave + j;
     if (rl >= r_end) break;  // uniform across the wave
     const int64_t t = b0 + rl;
     const uint4* xr = x + t * nc;
@@ -330,14 +332,14 @@ constexpr int64_t kFusedNormRows = 65536;
 
 template <int NCL>
 static hipError_t launch_fused(const void* x, const void* gamma, const float* rstd, const float* grad_h, int64_t T,
-                               float* grad_x, float* part, hipStream_t s) {
-  const dim3 g((unsigned)((T + 255) / 256)), b(256);
+                               int rpw, float* grad_x, float* part, hipStream_t s) {
+  const dim3 g((unsigned)((T + 4 * rpw - 1) / (4 * rpw))), b(256);
   if (grad_x)
     hipLaunchKernelGGL((rmsnorm_bwd_fused<NCL, true>), g, b, 0, s, (const uint4*)x, (const uint4*)gamma, rstd,
-                       (const float4*)grad_h, T, (float4*)grad_x, part);
+                       (const float4*)grad_h, T, rpw, (float4*)grad_x, part);
   else
     hipLaunchKernelGGL((rmsnorm_bwd_fused<NCL, false>), g, b, 0, s, (const uint4*)x, (const uint4*)gamma, rstd,
-                       (const float4*)grad_h, T, (float4*)nullptr, part);
+                       (const float4*)grad_h, T, rpw, (float4*)nullptr, part);
   return hipGetLastError();
 }
 
@@ -346,13 +348,19 @@ hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float
                                    hipStream_t s) {
   // Large calls at the widths whose rows stay in registers take grad_gamma's
   // block sums in the grad_x pass (with or without grad_x): one workgroup per
-  // 256 rows walks its rows in order, which pays once there are enough blocks
-  // to fill the chip. The choice depends on (T, d) only.
+  // block of rows walks its rows in order, which pays once there are enough
+  // blocks to fill the chip. The choice depends on (T, d) only.
   const bool fused = grad_gamma && (d == 2048 || d == 4096) && T >= kFusedNormRows;
+  // Rows per wave: 64, or more where that many blocks would not all be
+  // resident at once on a 256-CU MI355X (two workgroups per CU at d = 4096,
+  // four at 2048), which would leave a second round of a few blocks walking
+  // their rows alone. A constant, so the order depends on (T, d) only.
+  const int64_t resident = d == 2048 ? 1024 : 512;
+  const int rpw = (int)std::max<int64_t>(64, (T + 4 * resident - 1) / (4 * resident));
   if (fused && T > 0) {
     if ((T + 255) / 256 > 65535) return hipErrorInvalidValue;
-    const hipError_t e = d == 2048 ? launch_fused<4>(x, gamma, rstd, grad_h, T, grad_x, part, s)
-                                   : launch_fused<8>(x, gamma, rstd, grad_h, T, grad_x, part, s);
+    const hipError_t e = d == 2048 ? launch_fused<4>(x, gamma, rstd, grad_h, T, rpw, grad_x, part, s)
+                                   : launch_fused<8>(x, gamma, rstd, grad_h, T, rpw, grad_x, part, s);
     if (e != hipSuccess) return e;
   }
   if (T > 0 && grad_x && !fused) {
@@ -372,7 +380,7 @@ hipError_t launch_rmsnorm_backward(const void* x, const void* gamma, const float
     if (e != hipSuccess) return e;
   }
   if (grad_gamma) {
-    const int64_t n_blocks = (T + 255) / 256;
+    const int64_t n_blocks = fused ? (T + 4 * rpw - 1) / (4 * rpw) : (T + 255) / 256;
     if (n_blocks > 65535) return hipErrorInvalidValue;
     const unsigned gx = (unsigned)((d + 255) / 256);
     if (n_blocks > 0 && !fused) {
