@@ -170,12 +170,12 @@ def test_rmsnorm_degenerate_calls():
 
 
 @pytest.mark.parametrize("d,with_gamma,T", [(2048, True, 65536 + 77), (4096, False, 65536 + 77),
-                                            (4096, True, 131072 + 77)])
+                                            (4096, True, 131072 + 77), (2048, False, 262144 + 77)])
 def test_rmsnorm_backward_large_call_vs_oracle(d, with_gamma, T):
     """Calls of at least 65536 rows at d = 2048 / 4096 form grad_gamma's block
     sums in the grad_x pass (each wave's rows in order, then (q0 + q1) + (q2 +
-    q3) per block; above 131072 rows at d = 4096 a wave takes more than 64
-    rows): grad_gamma against the oracle within its bound, grad_x bitwise equal
+    q3) per block; above 131072 rows at d = 4096, 262144 at d = 2048, a wave
+    takes more than 64 rows): grad_gamma against the oracle within its bound, grad_x bitwise equal
     to the same rows evaluated alone (the smaller call's path) and to the
     oracle on sampled rows, and grad_gamma without grad_x the same bits."""
     print(f"case large T={T} d={d} gamma={with_gamma}", flush=True)
@@ -217,6 +217,6 @@ def test_rmsnorm_backward_large_call_vs_oracle(d, with_gamma, T):
     err_g = np.abs(gg.double().cpu().numpy() - dg)
     rg = (err_g / ((256 + T / 256 + 32) * U * mag_g + 1e-30)).max()
     err_x /= dx_max
-    print(f"[parity] large rmsnorm backward T={T} d={d}: grad_gamma max err/bound {rg:.3f}, "
+    print(f"[parity] large rmsnorm backward T={T} d={d}: grad_gamma max err/bound {rg:.2e}, "
           f"grad_x max rel err {err_x:.2e}")
     assert rg <= 1.0 and err_x <= 1e-5
