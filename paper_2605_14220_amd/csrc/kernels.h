@@ -62,6 +62,35 @@ struct GemmArgs {
   int32_t accumulate;
 };
 
+// K3 estimator of the correction ratio r = e^delta (Section 4.1), e^delta - 1
+// - delta, from the exact fp64 difference of two fp32 log-probabilities. In
+// fp64 the form expm1(delta) - delta loses about 2^-52 / |delta| of relative
+// accuracy to expm1's rounding (the subtraction itself is exact), which for
+// |delta| below 2^-5 a Taylor polynomial avoids: delta^2 (1/2 + delta/6 + ...
+// + delta^6/8!), whose first omitted term is below 2^-50 of the sum there.
+// Either way the fp64 value is within 2^-46 of K3 relative, so its one
+// rounding to fp32 is correct to within that of a correctly rounded K3.
+__device__ __forceinline__ double k3_of_delta(double d) {
+  if (__builtin_fabs(d) < 0.03125) {
+    double p = 1.0 / 40320.0;
+    p = __builtin_fma(p, d, 1.0 / 5040.0);
+    p = __builtin_fma(p, d, 1.0 / 720.0);
+    p = __builtin_fma(p, d, 1.0 / 120.0);
+    p = __builtin_fma(p, d, 1.0 / 24.0);
+    p = __builtin_fma(p, d, 1.0 / 6.0);
+    p = __builtin_fma(p, d, 0.5);
+    return (d * d) * p;
+  }
+  return expm1(d) - d;  // NaN stays NaN; delta = -inf gives +inf
+}
+
+// Truncated importance weight min(e^delta, C) (Section 4.2, Eq. 6) from the
+// exact fp64 difference, rounded once to fp32; a NaN ratio stays NaN.
+__device__ __forceinline__ float tis_weight(double d, float C) {
+  const double r = exp(d);
+  return (r > (double)C) ? C : (float)r;
+}
+
 int n_vocab_tiles(int V);
 int n_half_tiles(int V);
 

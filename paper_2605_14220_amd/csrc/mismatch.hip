@@ -1,6 +1,10 @@
 // Token-level mismatch statistics (Section 2 Eq. 1; Section 4.1 K3; Section 4.2
 // r_corr and the truncation of Eq. 6). Elementwise and HBM-bound: 8 bytes in,
 // up to 12 bytes out per token, 4 tokens per thread with 16-byte accesses.
+// Each statistic is formed in fp64 from the exact difference of the two fp32
+// inputs and rounded once to fp32, so K3 keeps its relative accuracy however
+// small the difference (an fp32 expm1(delta) - delta cancels to nothing near
+// delta ~ 1e-7, the typical size of an engine-to-engine discrepancy).
 
 #include "kernels.h"
 
@@ -12,11 +16,11 @@ struct Stats {
 };
 
 __device__ __forceinline__ Stats stats_of(float a, float b, float C) {
+  const double d = (double)a - (double)b;  // exact: two fp32 values differ by an fp64-representable amount
   Stats r;
-  r.delta = a - b;                          // log pi_a - log pi_b
-  r.k3 = expm1f(r.delta) - r.delta;         // (ratio - 1) - log ratio, ratio = e^delta
-  const float ratio = expf(r.delta);
-  r.w = (ratio > C) ? C : ratio;            // truncate above at C; NaN stays NaN
+  r.delta = (float)d;                      // log pi_a - log pi_b, rounded once
+  r.k3 = (float)k3_of_delta(d);            // (ratio - 1) - log ratio, ratio = e^delta
+  r.w = tis_weight(d, C);                  // ratio truncated above at C
   return r;
 }
 

@@ -32,7 +32,7 @@ __global__ __launch_bounds__(kSeqThreads) void seqstats_kernel(const float* __re
   double acc = 0.0;
   for (int64_t t = s0 + threadIdx.x; t < s1; t += kSeqThreads) {
     const double delta = (double)a[t] - (double)b[t];  // exact in fp64
-    acc += k3 ? expm1(delta) - delta : -delta;         // K3 = (r - 1) - log r, K1 = -log r; r = e^delta
+    acc += k3 ? k3_of_delta(delta) : -delta;           // K3 = (r - 1) - log r, K1 = -log r; r = e^delta
   }
   // each xor step adds the same two values in every lane pair, so all lanes agree
 #pragma unroll
@@ -53,8 +53,8 @@ __global__ __launch_bounds__(kSeqThreads) void seqstats_kernel(const float* __re
   if (weight) {
     const int k = keep_s;
     for (int64_t t = s0 + threadIdx.x; t < s1; t += kSeqThreads) {
-      const float r = expf(a[t] - b[t]);  // tim_mismatch's correction ratio and truncation
-      weight[t] = k ? ((r > C) ? C : r) : 0.f;
+      // tim_mismatch's correction ratio and truncation
+      weight[t] = k ? tis_weight((double)a[t] - (double)b[t], C) : 0.f;
     }
   }
 }
