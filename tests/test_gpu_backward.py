@@ -204,3 +204,40 @@ def test_degenerate_calls():
     print(f"[parity] uniform rows: max|grad_hidden - g (w_a - mean w)| = {err:.2e}")
     assert err <= 2.0 ** -8 * 2 * wf.abs().max().item() * gl.abs().max().item()
     assert (gw == 0).all()
+
+
+def test_persistent_backward_full_vocab():
+    """The backward at the headline shape (d = 4096, V = 151936) with micro-batches of 4352 tokens and a ragged
+    second one (T = 4613): every pass runs on the persistent grid (logit gradients: 594 x 17 tiles; grad_hidden:
+    16 x 17 tiles; grad_w: 16 x 594 tiles, a workgroup walking ~37 of them), and the second micro-batch's grad_w
+    pass resumes each tile from the value the first stored. Checked element by element against the oracle:
+    grad_w on the row of every sampled token plus 64 seeded vocabulary rows (the first, the last, the tail tile),
+    grad_hidden on 256 seeded rows (both micro-batches' edges included), each within the derived bound."""
+    T, d, V, tau, mb = 4613, 4096, 151936, 1.0, 4352
+    print(f"case T={T} d={d} V={V} mb={mb}", flush=True)
+    h, W = inputs(T, d, V, seed=31, w_std=0.02)
+    tok = random_tokens(T, V, 31)
+    lp, H, lse = tim.logprobs(h, W, tok, tau, lse=True)
+    gl, ge = _upstream(T, 31)
+    gh, gw = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H, grad_entropy=ge, micro_batch=mb)
+    torch.cuda.synchronize()
+    gh_n, gw_n = gh.double().cpu().numpy(), gw.double().cpu().numpy()
+    del gh, gw
+    print("[persistent backward] GPU done; oracle logit gradients of every row", flush=True)
+    dacc = oracle.logit_grads(bf16_bits(h), bf16_bits(W), tok.cpu().numpy(), tau, gl.cpu().double().numpy(),
+                              ge.cpu().double().numpy(), row_block=1024)
+    rng = np.random.default_rng(31)
+    vrows = np.unique(np.concatenate([tok.cpu().numpy().astype(np.int64), rng.choice(V, 61, replace=False),
+                                      [0, V - 1, V - 100]]))
+    hf = oracle.bf16_to_f64(bf16_bits(h))
+    da_v = np.ascontiguousarray(dacc[:, vrows])
+    t_all = (mb + 127) // 128 * 128 + (T - mb + 127) // 128 * 128  # the chain over both micro-batches' padded tokens
+    _bound_check(f"grad_w on {len(vrows)} vocabulary rows (persistent, resumed)", torch.as_tensor(gw_n[vrows]),
+                 da_v.T @ hf, np.abs(da_v).T @ np.abs(hf), t_all)
+    trows = np.unique(np.concatenate([rng.choice(T, 250, replace=False), [0, mb - 1, mb, T - 1, 255, 256]]))
+    wf = oracle.bf16_to_f64(bf16_bits(W))
+    da_t = dacc[trows]
+    del dacc
+    v_pad = (V + 255) // 256 * 256
+    _bound_check(f"grad_hidden on {len(trows)} rows (persistent)", torch.as_tensor(gh_n[trows]), da_t @ wf,
+                 np.abs(da_t) @ np.abs(wf), v_pad)
