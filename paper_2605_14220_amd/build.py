@@ -39,8 +39,7 @@ FLAGS = [
 
 
 def build(asm_dir: str | None = None, verbose: bool = False, defines=(), out: str = LIB) -> str:
-    """Compile the library. `defines` are NAME=VALUE pipeline-shape overrides
-    (TIM_NBUF, TIM_GROUP_V, TIM_LOAD_AUX, TIM_PERSISTENT, TIM_WIDE_WAVES); they never change results."""
+    """Compile the library (`defines`: extra NAME=VALUE preprocessor definitions passed to hipcc)."""
     if shutil.which(HIPCC) is None and not os.path.exists(HIPCC):
         raise RuntimeError(f"hipcc not found at {HIPCC}")
     tmp = out + ".tmp"
@@ -67,7 +66,7 @@ def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--asm", default=None, help="directory for -save-temps output")
     ap.add_argument("-v", "--verbose", action="store_true")
-    ap.add_argument("-D", dest="defines", action="append", default=[], help="NAME=VALUE pipeline override")
+    ap.add_argument("-D", dest="defines", action="append", default=[], help="NAME=VALUE preprocessor definition")
     ap.add_argument("-o", dest="out", default=LIB)
     args = ap.parse_args(argv)
     print(build(args.asm, args.verbose, args.defines, args.out))

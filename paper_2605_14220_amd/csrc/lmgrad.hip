@@ -46,7 +46,7 @@ struct EpiDlogits {
   using Args = DlogitsArgs;
   static constexpr bool kTokens = true;
   static constexpr bool kCoef = true;
-  static constexpr int kGroupA = TIM_GROUP_V;
+  static constexpr int kGroupA = kGroupV;
   static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
@@ -107,7 +107,7 @@ struct EpiStore {
   using Args = GemmArgs;
   static constexpr bool kTokens = false;
   static constexpr bool kCoef = false;
-  static constexpr int kGroupA = TIM_STORE_GROUP;
+  static constexpr int kGroupA = kStoreGroup;
   static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }

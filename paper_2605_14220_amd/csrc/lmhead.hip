@@ -232,7 +232,7 @@ struct EpiPartials {
   using Args = LmHeadArgs;
   static constexpr bool kTokens = !DUMP;
   static constexpr bool kCoef = false;
-  static constexpr int kGroupA = TIM_GROUP_V;
+  static constexpr int kGroupA = kGroupV;
   static constexpr int kNV = NV;
   template <int BT>
   static constexpr int scratch_bytes() { return NV == 2 ? 7 * BT * 4 : 0; }
@@ -415,14 +415,8 @@ hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, h
   switch (rows_per_wg) {
     case 64: return dump ? launch_partials_t<1, 2, false, true>(a, false, s) : launch_partials_t<1, 2, false, false>(a, false, s);
     case 128: return dump ? launch_partials_t<2, 2, false, true>(a, false, s) : launch_partials_t<2, 2, false, false>(a, false, s);
-    default: {
-      const bool pers = TIM_PERSISTENT != 0;
-#if TIM_WIDE_WAVES
-      return dump ? launch_partials_t<2, 4, false, true>(a, pers, s) : launch_partials_t<2, 4, false, false>(a, pers, s);
-#else
-      return dump ? launch_partials_t<4, 2, false, true>(a, pers, s) : launch_partials_t<4, 2, false, false>(a, pers, s);
-#endif
-    }
+    default:  // 256-row tiles, 8 waves; full-size launches persistent
+      return dump ? launch_partials_t<2, 4, false, true>(a, true, s) : launch_partials_t<2, 4, false, false>(a, true, s);
   }
 }
 

@@ -39,27 +39,12 @@ struct rsrc_t {
 };
 #endif
 
-// Compile-time launch and pipeline shape. None of these changes the
-// arithmetic: the hidden dimension is accumulated in the same ascending
-// 32-element MFMA steps whatever the buffer count, LDS swizzle or tile order.
-#ifndef TIM_NBUF
-#define TIM_NBUF 2         // LDS stage buffers: a power of two >= 2 (as many as fit, up to this)
-#endif
-#ifndef TIM_GROUP_V
-#define TIM_GROUP_V 4      // vocab tiles per group in the workgroup -> tile order
-#endif
-#ifndef TIM_STORE_GROUP
-#define TIM_STORE_GROUP 8  // A tiles per group in the tile order of the plain products
-#endif
-#ifndef TIM_LOAD_AUX
-#define TIM_LOAD_AUX 0     // cache-policy bits of the global->LDS loads (gfx950 sc0=1, nt=2, sc1=16)
-#endif
-#ifndef TIM_PERSISTENT
-#define TIM_PERSISTENT 1   // full-size launches: one workgroup per CU looping over tiles
-#endif
-#ifndef TIM_WIDE_WAVES
-#define TIM_WIDE_WAVES 1   // 256-row tiles: 8 waves of 128x64 (2 per SIMD); 0 = 4 waves of 128x128
-#endif
+// Launch and pipeline shape. None of these changes the arithmetic: the
+// hidden dimension is accumulated in the same ascending 32-element MFMA steps
+// whatever the buffer count, LDS swizzle or tile order.
+constexpr int kMaxNBuf = 2;     // LDS stage buffers per workgroup (a power of two, as many as fit up to this)
+constexpr int kGroupV = 4;      // vocab tiles per group in the LM head's workgroup -> tile order
+constexpr int kStoreGroup = 8;  // A tiles per group in the tile order of the plain products
 
 constexpr int kKS = 64;                  // hidden-dimension elements per LDS stage
 constexpr int kRowBytes = kKS * 2;       // bytes of one row in one stage
@@ -96,7 +81,7 @@ struct Shape {
       NV == 1 ? (FIT2 >= 3 ? 3 : FIT2)
               : ((WT == 2 && NTB <= 2 && !SPLITK4 && (80 * 1024) / TL::kStageBytes >= 2) ? 2 : 1);
   static constexpr int FIT = (160 * 1024 / PER_CU) / TL::kStageBytes;
-  static constexpr int CAP = FIT < TIM_NBUF ? FIT : TIM_NBUF;
+  static constexpr int CAP = FIT < kMaxNBuf ? FIT : kMaxNBuf;
   // a power of two, so that it divides the stage count
   static constexpr int NBUF = CAP >= 8 ? 8 : CAP >= 4 ? 4 : 2;
   static_assert(FIT >= 2, "double buffering at least");
@@ -250,10 +235,10 @@ __device__ __forceinline__ void request_load(unsigned char* buf, rsrc_t wr, rsrc
   constexpr int kWB = Tile<NTB, WT, NV>::kWB;
   if (q < WB)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + (wave * WB + q) * 1024), 16, pl.w_off[q], soff, 0,
-                                             TIM_LOAD_AUX);
+                                             0);
   else
     __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + kWB + (wave * (L - WB) + (q - WB)) * 1024), 16,
-                                             pl.h_off[q - WB], soff, 0, TIM_LOAD_AUX);
+                                             pl.h_off[q - WB], soff, 0, 0);
 #endif
 }
 
