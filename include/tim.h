@@ -111,6 +111,34 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
                         float* logp, float* entropy, float* lse,
                         void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/* Size of the device scratch array behind tim_logprobs_noalloc: 64 MiB, held
+ * by every GPU the library runs on until the process ends. */
+#define TIM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* tim_logprobs for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc. Same
+ * arguments, outputs and errors as tim_logprobs, without the workspace: the
+ * softmax partials go to a file-scope device array of
+ * TIM_NOALLOC_SCRATCH_BYTES per GPU, whose address is looked up once per
+ * device on that device's first call. The call allocates nothing (no
+ * hipMalloc / hipFree, no allocating library routine) and gives exactly the
+ * bits of tim_logprobs on the same arguments.
+ *
+ * Limit: tim_logprobs_workspace_size(T, d, V, mode, micro_batch) must not
+ * exceed TIM_NOALLOC_SCRATCH_BYTES, else TIM_ERR_WORKSPACE before anything is
+ * enqueued (at V = 151936: up to 7061 rows per launch -- a rollout batch of
+ * that many rows, or training micro-batches of at most that many tokens).
+ * TIM_ERR_HIP if the device array's address cannot be obtained.
+ *
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * partials (each launch writes every partial it reads, so nothing needs
+ * clearing). Calls that overlap in time on one GPU (on different streams or
+ * from different host threads) race on the array: serialise them. */
+tim_status tim_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens,
+                                int64_t T, int32_t d, int32_t V, float temperature,
+                                int32_t mode, int64_t micro_batch, int32_t order,
+                                float* logp, float* entropy, float* lse, hipStream_t stream);
+
 /* The two stages of tim_logprobs, for callers that schedule them themselves
  * (a profiler timing one kernel, or a vocabulary-sharded deployment that
  * exchanges partials between the stages). tim_logprobs over one launch's rows

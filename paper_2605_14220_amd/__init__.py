@@ -70,6 +70,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.tim_logprobs.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
                                  c.c_float, c.c_int32, c.c_int64, c.c_int32, c.c_void_p, c.c_void_p,
                                  c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p]
+    lib.tim_logprobs_noalloc.restype = c.c_int
+    lib.tim_logprobs_noalloc.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32, c.c_int32,
+                                         c.c_float, c.c_int32, c.c_int64, c.c_int32, c.c_void_p, c.c_void_p,
+                                         c.c_void_p, c.c_void_p]
     lib.tim_logprobs_partials.restype = c.c_int
     lib.tim_logprobs_partials.argtypes = [c.c_void_p, c.c_void_p, c.c_void_p, c.c_int64, c.c_int32,
                                           c.c_int32, c.c_float, c.c_int32, c.c_int32, c.c_void_p,
@@ -178,6 +182,40 @@ def logprobs(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor, 
     _check(lib.tim_logprobs(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature),
                             int(mode), int(micro_batch), int(order), _ptr(lp), _ptr(ent), _ptr(ls),
                             _ptr(workspace), ws_bytes, _stream(dev)))
+    return lp, ent, ls
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TIM_NOALLOC_SCRATCH_BYTES
+
+
+def logprobs_noalloc(hidden: torch.Tensor, w_vocab: torch.Tensor, tokens: torch.Tensor, temperature: float = 1.0,
+                     mode: Mode = Mode.TRAINING, micro_batch: int = 0, order: Order = Order.INVARIANT,
+                     out: tuple | None = None):
+    """tim_logprobs_noalloc: logprobs() with the partials in the library's per-GPU device array instead of a
+    workspace (the call allocates no device memory; pass `out` = (logp, entropy or None, lse or None) to keep
+    the binding from allocating the outputs). Needs workspace_size(T, d, V, mode, micro_batch) <=
+    NOALLOC_SCRATCH_BYTES."""
+    lib = load_library()
+    if hidden.dtype != torch.bfloat16 or w_vocab.dtype != torch.bfloat16:
+        raise TypeError("tim.logprobs_noalloc: hidden and w_vocab must be bfloat16")
+    if tokens.dtype != torch.int32:
+        raise TypeError("tim.logprobs_noalloc: tokens must be int32")
+    if hidden.dim() != 2 or w_vocab.dim() != 2 or hidden.shape[1] != w_vocab.shape[1]:
+        raise ValueError("tim.logprobs_noalloc: hidden [T, d] and w_vocab [V, d] must share d")
+    T, d = hidden.shape
+    V = w_vocab.shape[0]
+    if tokens.shape != (T,):
+        raise ValueError("tim.logprobs_noalloc: tokens must be [T]")
+    _require_gpu(hidden, w_vocab, tokens)
+    dev = hidden.device
+    if out is None:
+        out = (torch.empty(T, dtype=torch.float32, device=dev), torch.empty(T, dtype=torch.float32, device=dev),
+               None)
+    lp, ent, ls = out
+    _require_gpu(lp, ent, ls)
+    _check(lib.tim_logprobs_noalloc(_ptr(hidden), _ptr(w_vocab), _ptr(tokens), T, d, V, float(temperature),
+                                    int(mode), int(micro_batch), int(order), _ptr(lp), _ptr(ent), _ptr(ls),
+                                    _stream(dev)))
     return lp, ent, ls
 
 

@@ -9,6 +9,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 
 #include "kernels.h"
@@ -31,24 +32,32 @@ inline int row_tile_for(int64_t rows, int32_t mode, bool splitk4) {
   return rt;
 }
 
-}  // namespace
+// Device scratch of tim_logprobs_noalloc (one copy per GPU, for the life of
+// the process). Host code never passes this name to a kernel or a copy: on
+// the host it is only a stand-in; its device address comes from
+// hipGetSymbolAddress, once per device (scratch_on_current_device).
+__device__ __align__(256) unsigned char scratch[TIM_NOALLOC_SCRATCH_BYTES];
 
-extern "C" {
-
-size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch) {
-  if (T <= 0 || tim::check_shape(T, d, V, TIM_ORDER_INVARIANT) != TIM_OK) return 0;
-  if (!tim::valid_mode(mode) || micro_batch < 0) return 0;
-  return tim::workspace_bytes(T, V, mode, micro_batch);
+// Address of `scratch` on the current device, looked up on the device's first
+// call with that device current and kept per device (host threads may race on
+// a first call; each looks up the same address). nullptr if the lookup fails.
+void* scratch_on_current_device() {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void*> cache[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  void* p = cache[dev].load(std::memory_order_acquire);
+  if (p != nullptr) return p;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+  cache[dev].store(p, std::memory_order_release);
+  return p;
 }
 
-tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,
-                        int32_t d, int32_t V, float temperature, int32_t mode, int64_t micro_batch,
-                        int32_t order, float* logp, float* entropy, float* lse, void* workspace,
-                        size_t workspace_bytes, hipStream_t stream) {
-  tim_status st = tim::validate_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode,
-                                         micro_batch, order, logp, workspace, workspace_bytes);
-  if (st != TIM_OK || T == 0) return st;
-
+// The launches of tim_logprobs over validated arguments, partials in `workspace`.
+tim_status run_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T, int32_t d,
+                        int32_t V, float temperature, int32_t mode, int64_t micro_batch, int32_t order, float* logp,
+                        float* entropy, float* lse, void* workspace, hipStream_t stream) {
+  tim_status st = TIM_OK;
   const bool splitk4 = order == TIM_ORDER_SPLITK4;
   const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
   const int tb = row_tile_for(step, mode, splitk4);
@@ -83,6 +92,39 @@ tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
     if (st != TIM_OK) return st;
   }
   return TIM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch) {
+  if (T <= 0 || tim::check_shape(T, d, V, TIM_ORDER_INVARIANT) != TIM_OK) return 0;
+  if (!tim::valid_mode(mode) || micro_batch < 0) return 0;
+  return tim::workspace_bytes(T, V, mode, micro_batch);
+}
+
+tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,
+                        int32_t d, int32_t V, float temperature, int32_t mode, int64_t micro_batch,
+                        int32_t order, float* logp, float* entropy, float* lse, void* workspace,
+                        size_t workspace_bytes, hipStream_t stream) {
+  const tim_status st = tim::validate_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode,
+                                               micro_batch, order, logp, workspace, workspace_bytes);
+  if (st != TIM_OK || T == 0) return st;
+  return run_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode, micro_batch, order, logp, entropy, lse,
+                      workspace, stream);
+}
+
+tim_status tim_logprobs_noalloc(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,
+                                int32_t d, int32_t V, float temperature, int32_t mode, int64_t micro_batch,
+                                int32_t order, float* logp, float* entropy, float* lse, hipStream_t stream) {
+  const tim_status st = tim::validate_logprobs_noalloc(hidden, w_vocab, tokens, T, d, V, temperature, mode,
+                                                       micro_batch, order, logp);
+  if (st != TIM_OK || T == 0) return st;
+  void* ws = scratch_on_current_device();
+  if (ws == nullptr) return TIM_ERR_HIP;
+  return run_logprobs(hidden, w_vocab, tokens, T, d, V, temperature, mode, micro_batch, order, logp, entropy, lse,
+                      ws, stream);
 }
 
 tim_status tim_logprobs_partials(const void* hidden, const void* w_vocab, const int32_t* tokens,
@@ -315,7 +357,7 @@ const char* tim_status_string(tim_status s) {
     case TIM_ERR_NULL: return "TIM_ERR_NULL: a required pointer is NULL";
     case TIM_ERR_SHAPE: return "TIM_ERR_SHAPE: T, d or V out of range";
     case TIM_ERR_VALUE: return "TIM_ERR_VALUE: bad temperature, C, mode, order, micro_batch or alignment";
-    case TIM_ERR_WORKSPACE: return "TIM_ERR_WORKSPACE: workspace missing, misaligned or too small";
+    case TIM_ERR_WORKSPACE: return "TIM_ERR_WORKSPACE: workspace missing, misaligned or too small (or, without one, beyond the device scratch array)";
     case TIM_ERR_HIP: return "TIM_ERR_HIP: a HIP call or kernel launch failed";
   }
   return "unknown tim_status";

@@ -45,10 +45,11 @@ inline size_t workspace_bytes(int64_t T, int32_t V, int32_t mode, int64_t micro_
   return (size_t)rows * (size_t)per_row * 16u;
 }
 
-inline tim_status validate_logprobs(const void* hidden, const void* w, const int32_t* tokens,
-                                    int64_t T, int32_t d, int32_t V, float temperature,
-                                    int32_t mode, int64_t micro_batch, int32_t order,
-                                    const float* logp, const void* ws, size_t ws_bytes) {
+// Every argument of tim_logprobs but the workspace.
+inline tim_status validate_logprobs_args(const void* hidden, const void* w, const int32_t* tokens,
+                                         int64_t T, int32_t d, int32_t V, float temperature,
+                                         int32_t mode, int64_t micro_batch, int32_t order,
+                                         const float* logp) {
   if (T < 0) return TIM_ERR_SHAPE;
   if (T == 0) return TIM_OK;
   if (!hidden || !w || !tokens || !logp) return TIM_ERR_NULL;
@@ -57,8 +58,29 @@ inline tim_status validate_logprobs(const void* hidden, const void* w, const int
   if (!positive_finite(temperature)) return TIM_ERR_VALUE;
   if (!valid_mode(mode) || !valid_order(order) || micro_batch < 0) return TIM_ERR_VALUE;
   if (!aligned16(hidden) || !aligned16(w)) return TIM_ERR_VALUE;
+  return TIM_OK;
+}
+
+inline tim_status validate_logprobs(const void* hidden, const void* w, const int32_t* tokens,
+                                    int64_t T, int32_t d, int32_t V, float temperature,
+                                    int32_t mode, int64_t micro_batch, int32_t order,
+                                    const float* logp, const void* ws, size_t ws_bytes) {
+  const tim_status s = validate_logprobs_args(hidden, w, tokens, T, d, V, temperature, mode, micro_batch, order, logp);
+  if (s != TIM_OK || T == 0) return s;
   if (!ws || !aligned16(ws) || ws_bytes < workspace_bytes(T, V, mode, micro_batch))
     return TIM_ERR_WORKSPACE;
+  return TIM_OK;
+}
+
+// tim_logprobs_noalloc: the arguments, then whether its partials fit the
+// device scratch array (checked before the array's address is looked up).
+inline tim_status validate_logprobs_noalloc(const void* hidden, const void* w, const int32_t* tokens,
+                                            int64_t T, int32_t d, int32_t V, float temperature,
+                                            int32_t mode, int64_t micro_batch, int32_t order,
+                                            const float* logp) {
+  const tim_status s = validate_logprobs_args(hidden, w, tokens, T, d, V, temperature, mode, micro_batch, order, logp);
+  if (s != TIM_OK || T == 0) return s;
+  if (workspace_bytes(T, V, mode, micro_batch) > TIM_NOALLOC_SCRATCH_BYTES) return TIM_ERR_WORKSPACE;
   return TIM_OK;
 }
 

@@ -38,7 +38,8 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == ["tim_logit_grads", "tim_logits", "tim_logprobs", "tim_logprobs_backward",
-                     "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_partials",
+                     "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_noalloc",
+                     "tim_logprobs_partials",
                      "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_ppo_loss", "tim_rmsnorm",
                      "tim_rmsnorm_backward", "tim_rmsnorm_backward_workspace_size", "tim_status_string"]
 
@@ -129,6 +130,47 @@ def test_logprobs_T_zero_is_noop_even_with_null_pointers(lib):
 ])
 def test_logprobs_rejects(lib, kw, expect):
     assert _lp(lib, **kw) == expect
+
+
+def _lp_noalloc(lib, hidden=FAKE, w=FAKE, tokens=FAKE, T=8, d=256, V=4096, tau=1.0, mode=1, mb=0, order=0,
+                logp=FAKE):
+    return lib.tim_logprobs_noalloc(hidden, w, tokens, T, d, V, tau, mode, mb, order, logp, None, None, None)
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(T=0, hidden=None, w=None, tokens=None, logp=None), Status.OK),
+    (dict(T=-1), Status.ERR_SHAPE),
+    (dict(hidden=None), Status.ERR_NULL),
+    (dict(logp=None), Status.ERR_NULL),
+    (dict(d=200), Status.ERR_SHAPE),
+    (dict(tau=0.0), Status.ERR_VALUE),
+    (dict(mode=3), Status.ERR_VALUE),
+    (dict(w=FAKE_MIS), Status.ERR_VALUE),
+    # partials beyond the 64 MiB device array: at V = 151936 (594 tiles of 16 B per row) 7061 rows fit, 7062 not
+    (dict(T=7062, d=4096, V=151936, mode=0), Status.ERR_WORKSPACE),
+    (dict(T=20000, d=4096, V=151936, mode=1, mb=7062), Status.ERR_WORKSPACE),
+    (dict(T=20000, d=4096, V=151936, mode=1, mb=0), Status.ERR_WORKSPACE),
+    (dict(T=1, d=128, V=2048 * 256, mode=1), Status.ERR_HIP),
+])
+def test_logprobs_noalloc_rejects_on_the_host(lib, kw, expect):
+    """Every argument check of tim_logprobs_noalloc, including its scratch limit, runs on the host before any
+    HIP call (the last case passes them and fails only at the device lookup, as there is no GPU here)."""
+    if expect == Status.ERR_HIP and _has_gpu():
+        pytest.skip("a GPU is present: the call would launch")
+    assert _lp_noalloc(lib, **kw) == expect
+
+
+def _has_gpu():
+    import torch
+    return torch.cuda.is_available()
+
+
+def test_noalloc_scratch_limit_matches_the_header():
+    text = open(HEADER).read()
+    assert "#define TIM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)" in text
+    assert tim.NOALLOC_SCRATCH_BYTES == 64 << 20
+    # 7061 rows of partials at V = 151936 fit, the next row does not
+    assert 7061 * 594 * 16 <= tim.NOALLOC_SCRATCH_BYTES < 7062 * 594 * 16
 
 
 def test_logprobs_error_precedence(lib):
