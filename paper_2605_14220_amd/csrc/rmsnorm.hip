@@ -13,12 +13,15 @@
 //
 // Backward, with G = dL/dh (fp32) and the casts passed straight through:
 //   dx_k = r g_k G_k - (r^3 s / d) x_k,   s = sum_j G_j g_j x_j   (one wavefront per row)
-//   dg_k = sum_t G_tk x_tk r_t   as fixed-order column sums over blocks of 256
-//          rows, then over the blocks in order (no atomics). Within a block the
-//          rows go in order, except in calls of at least 65536 rows of width
-//          2048 or 4096, whose grad_x pass also forms the block sums: there each
-//          quarter of 64 rows goes in order and the quarters combine as
-//          (q0 + q1) + (q2 + q3).
+//   dg_k = sum_t G_tk x_tk r_t   as fixed-order column sums over blocks of
+//          rows, then over the blocks in order (no atomics). Blocks are 256
+//          rows whose rows go in order, except in calls of at least 65536 rows
+//          of width 2048 or 4096, whose grad_x pass also forms the block sums:
+//          there a block is 4 rpw rows, rpw = max(64, ceil(T / (4 R))) with
+//          R = 1024 at d = 2048 and 512 at d = 4096 (the blocks a 256-CU chip
+//          holds at once), each quarter of rpw rows goes in order and the
+//          quarters combine as (q0 + q1) + (q2 + q3). The order so depends on
+//          (T, d) only.
 // Each is one HBM pass over the rows; the norm costs ~0.2% of the LM head it
 // feeds, so it runs as its own launch ahead of the head instead of inside the
 // head's MFMA loop, which would repeat it once per vocabulary tile and add
