@@ -202,3 +202,60 @@ def test_decode_128_row_tiles_full_size():
     ref_lp, ref_H = oracle_rows(h, W, tok, 1.0, rows=rows)
     check_close("decode-128 logp", trn[0], ref_lp, TOL_LOGP, rows=rows)
     check_close("decode-128 entropy", trn[1], ref_H, TOL_ENT, rows=rows)
+
+
+
+@pytest.mark.parametrize("d", [128, 256, 384, 640])
+@pytest.mark.parametrize("V", [1, 129, 383, 4096 + 77, 4096 + 200, 600 * 256])
+@pytest.mark.parametrize("T", [129, 160, 193, 255, 256])
+def test_decode_129_256_bitwise_equal_training(d, V, T):
+    """Decode batches of 129..256 rows (whole tiles, one 256-row tile,
+    persistent): hidden sizes of 2 .. 10 stages, row tiles cut by the batch,
+    every kind of vocabulary tail. Bitwise equal to the training path, and
+    within tolerance of the oracle at small V."""
+    print(f"case decode 129..256 d={d} V={V} T={T}", flush=True)
+    h, W = inputs(T, d, V, seed=(V + 7 * T + d) % 1000, w_std=0.1)
+    tok = _tokens(T, V, seed=V + T + d)
+    dec, per_row = _decode(h, W, tok, 0.7)
+    assert per_row == -(-V // 256)
+    trn = tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, lse=True)
+    _same(dec, trn)
+    if V <= 4096 + 200 and d <= 256:
+        ref_lp, ref_H = oracle_rows(h, W, tok, 0.7)
+        check_close(f"decode 129..256 logp d={d} V={V}", dec[0], ref_lp, TOL_LOGP)
+        check_close(f"decode 129..256 entropy d={d} V={V}", dec[1], ref_H, TOL_ENT)
+
+
+def test_decode_129_256_full_size():
+    """d = 4096, V = 151936, decode batches of 129..256 rows (several tiles per
+    workgroup): bitwise equal to the training path, and to the oracle on
+    sampled rows of every row wave."""
+    T, d, V = 256, 4096, 151936
+    h, W = inputs(T, d, V, seed=47, w_std=0.02)
+    tok = _tokens(T, V, seed=47)
+    trn = tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING, lse=True)
+    for n in (129, 200, 256):
+        dec, per_row = _decode(h[:n].contiguous(), W, tok[:n].contiguous(), 1.0)
+        assert per_row == 594
+        for x, y in zip(dec, trn):
+            assert bits_equal(x, y[:n])
+    rows = [0, 1, 31, 32, 100, 128, 129, 160, 199, 224, 255]
+    ref_lp, ref_H = oracle_rows(h, W, tok, 1.0, rows=rows)
+    check_close("decode 129..256 logp", trn[0], ref_lp, TOL_LOGP, rows=rows)
+    check_close("decode 129..256 entropy", trn[1], ref_H, TOL_ENT, rows=rows)
+
+
+def test_decode_repeated_calls_identical():
+    """Repeated decode calls of 129..224 rows (row waves of the 256-row tile
+    with no rows) at several hidden sizes return the same bits every time, and
+    those of the training path."""
+    V = 4096 + 200
+    for d in (256, 384, 640):
+        for T in (129, 160, 193):
+            print(f"case repeated d={d} T={T}", flush=True)
+            h, W = inputs(T, d, V, seed=T + d, w_std=0.1)
+            tok = _tokens(T, V, seed=T + d)
+            trn = tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, lse=True)
+            for _ in range(4):
+                dec, _ = _decode(h, W, tok, 0.7)
+                _same(dec, trn)
