@@ -18,7 +18,9 @@ sequence-level statistics, the backward of the fused log-prob over the same
 stream (logit gradients, grad_hidden, grad_w), and the small (d = 2048, one
 packed call) and long (d = 5120, tau = 0.7, micro-batches of 32768, plus its
 rollout pass in decode batches of 64, checked bit for bit against training)
-workloads' own rates. The oracle's parity on its sample is asserted (1e-3).
+workloads' own rates, and the vendor GEMM (hipBLASLt) alone on the shapes of
+the head's three contractions as a practical ceiling measured in the same run.
+The oracle's parity on its sample is asserted (1e-3).
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 
@@ -331,6 +333,54 @@ def other_workload(name, steps, decode_rows=0):
     return r
 
 
+def vendor_gemm_reference(dev, d, V, rows, reps=5):
+    """The vendor GEMM (hipBLASLt through torch.mm, bf16 in, bf16 out) alone on the shapes of the head's
+    contractions at one micro-batch: the forward's logits h @ W^T (K = d; the fused kernel does the softmax on
+    top), and the backward's grad_hidden = dlogits @ W (K = V padded to 256) and grad_w = dlogits^T @ h (K =
+    rows, dlogits^T contiguous, as the backward stages it). A practical ceiling measured on the same box in the
+    same run, not part of the path; median of `reps` timed calls after one untimed."""
+    import torch
+    import numpy as np
+    vp = -(-V // 256) * 256
+    g = torch.Generator(device=dev).manual_seed(5)
+    h = torch.empty(rows, d, device=dev, dtype=torch.bfloat16).normal_(generator=g)
+    W = torch.empty(vp, d, device=dev, dtype=torch.bfloat16).normal_(0.0, 0.02, generator=g)
+    out = {}
+
+    def timed(name, fn, flop):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        tf = flop / (ms / 1e3) / 1e12
+        out[name] = {"ms": ms, "achieved": tf, "frac": tf / PEAK_BF16_TFLOPS}
+        log(f"[bench] vendor GEMM {name}: {ms:.3f} ms, {tf:.1f} TFLOP/s = {tf / PEAK_BF16_TFLOPS:.1%} of bf16 peak")
+
+    logits = torch.empty(rows, V, device=dev, dtype=torch.bfloat16)
+    timed("forward_logits", lambda: torch.mm(h, W[:V].t(), out=logits), 2.0 * rows * V * d)
+    del logits
+    dl = torch.empty(rows, vp, device=dev, dtype=torch.bfloat16).normal_(0.0, 0.01, generator=g)
+    gh = torch.empty(rows, d, device=dev, dtype=torch.bfloat16)
+    timed("grad_hidden", lambda: torch.mm(dl, W, out=gh), 2.0 * rows * vp * d)
+    dlt = dl.t().contiguous()
+    del dl, gh
+    gw = torch.empty(vp, d, device=dev, dtype=torch.bfloat16)
+    timed("grad_w", lambda: torch.mm(dlt, h, out=gw), 2.0 * rows * vp * d)
+    del dlt, gw, h, W
+    torch.cuda.empty_cache()
+    out["note"] = ("hipBLASLt via torch.mm on the same shapes (micro-batch rows), plain GEMM without the fused "
+                   "softmax / gradient epilogues: the practical MFMA ceiling of these contractions on this box")
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -345,6 +395,8 @@ def main(argv=None):
                     help="skip the backward measurement")
     ap.add_argument("--no-others", dest="others", action="store_false",
                     help="skip the small and long workloads")
+    ap.add_argument("--no-vendor", dest="vendor", action="store_false",
+                    help="skip the vendor GEMM reference on the same shapes")
     args = ap.parse_args(argv)
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: this path runs on a single GPU "
@@ -641,6 +693,11 @@ def main(argv=None):
         others = {"small": other_workload("small", steps=5),
                   "long": other_workload("long", steps=3, decode_rows=CONFIGS["long"].rollout_batch)}
 
+    vendor = None
+    if args.vendor:
+        torch.cuda.empty_cache()
+        vendor = vendor_gemm_reference(dev, d, V, mb)
+
     out = {
         "metric": METRIC,
         "value": tok_per_s,
@@ -675,6 +732,7 @@ def main(argv=None):
         "backward": bwd,
         "rmsnorm": norm,
         "ppo_loss": ppo,
+        "vendor_gemm_reference": vendor,
     }
     print(json.dumps(out), flush=True)
 
