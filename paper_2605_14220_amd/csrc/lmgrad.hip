@@ -69,6 +69,7 @@ struct EpiDlogits {
     const float inv_tau = a.inv_tau;
     const int64_t vlane = v0 + wv * 128 + 4 * g;
     const bool full = v0 + kVocabTile <= a.V;
+    const int lim = a.V - (int)vlane;  // entries past V: bi * 16 + r >= lim (tail tile only)
     uint16_t* out = (uint16_t*)a.dacc;
 #pragma unroll
     for (int bj = 0; bj < NJ; ++bj) {
@@ -77,7 +78,8 @@ struct EpiDlogits {
       if (tg >= a.rows) continue;
       const f32x4 c = coef_lds[t_loc];
       const float lse = c[0], alpha = c[1], beta = c[2], gamma = c[3];
-      const int64_t tl = (int64_t)tok_lds[t_loc] - vlane;  // the token's offset from this lane's first entry
+      // the token's offset from this lane's first entry (both below 2^31)
+      const int tl = tok_lds[t_loc] - (int)vlane;
       uint16_t* row = out + tg * a.ld + vlane;
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
@@ -90,7 +92,7 @@ struct EpiDlogits {
           const float p = exp2_hw(q * kLog2e);
           const float pw = p * __builtin_fmaf(beta, q, alpha);
           float dv = (tl == bi * 16 + r) ? gamma - pw : -pw;
-          if (!full && vlane + bi * 16 + r >= a.V) dv = 0.f;
+          if (!full && bi * 16 + r >= lim) dv = 0.f;
           o[r] = dv;
         }
         *(uint2*)(row + bi * 16) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
@@ -118,14 +120,16 @@ struct EpiStore {
   __device__ static void init(const Args& a, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], int wave, int lane) {
     const int wv = wave & 1, wt = wave >> 1;
     const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
+    const int64_t lim64 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
+    const int lim = lim64 > 256 ? 256 : (int)lim64;
 #pragma unroll
     for (int bj = 0; bj < 2 * NTB; ++bj) {
       const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
         const int64_t i0 = i_lane + bi * 16;
-        acc[bi][bj] = (a.accumulate && jr < a.b_rows && i0 < a.a_rows) ? *(const f32x4*)(a.out + jr * a.ldo + i0)
-                                                                      : f32x4{};
+        acc[bi][bj] = (a.accumulate && jr < a.b_rows && bi * 16 < lim) ? *(const f32x4*)(a.out + jr * a.ldo + i0)
+                                                                     : f32x4{};
       }
     }
   }
@@ -134,6 +138,8 @@ struct EpiStore {
                                   const int*, const f32x4*, int wave, int lane) {
     const int wv = wave & 1, wt = wave >> 1;
     const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
+    const int64_t lim64 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
+    const int lim = lim64 > 256 ? 256 : (int)lim64;
 #pragma unroll
     for (int bj = 0; bj < 2 * NTB; ++bj) {
       const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
@@ -141,7 +147,7 @@ struct EpiStore {
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
         const int64_t i0 = i_lane + bi * 16;
-        if (i0 < a.a_rows) *(f32x4*)(a.out + jr * a.ldo + i0) = acc[bi][bj];
+        if (bi * 16 < lim) *(f32x4*)(a.out + jr * a.ldo + i0) = acc[bi][bj];
       }
     }
   }

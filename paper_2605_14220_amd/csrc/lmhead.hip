@@ -60,6 +60,21 @@ __device__ __forceinline__ MSU merge2(MSU a, MSU b) {
   return r;
 }
 
+// z[i] for the i with 16 (i / 4) + i % 4 == tl (there is one: tl < 128,
+// tl % 16 < 4), as a chain of compare-selects. Each compare takes its own
+// opaque copy of tl, so none is hoisted ahead of the chain (which would hold
+// all 32 conditions in scalar registers at once).
+__device__ __forceinline__ float select_entry(const float (&z)[32], int tl) {
+  float zf = 0.f;
+#pragma unroll
+  for (int i = 0; i < 32; ++i) {
+    int t = tl;
+    asm volatile("" : "+v"(t));
+    if ((i >> 2) * 16 + (i & 3) == t) zf = z[i];
+  }
+  return zf;
+}
+
 // One tile's per-row results from its accumulators. Each wave holds 128 of
 // the tile's 256 vocabulary entries of its rows: for row block bj, lane l holds
 // row (l % 16) and, in register r of W block bi, the entry
@@ -110,9 +125,10 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
       for (int i = 0; i < 32; ++i) z[i] = z[i] * inv_tau;
     }
     if (!full) {
+      const int lim = (int)(V - vlane);  // entries past V: (i / 4) 16 + i % 4 >= lim (32-bit: V < 2^31)
 #pragma unroll
       for (int i = 0; i < 32; ++i)
-        if (vlane + (i >> 2) * 16 + (i & 3) >= V) z[i] = kNegInf;
+        if ((i >> 2) * 16 + (i & 3) >= lim) z[i] = kNegInf;
     }
     if constexpr (DUMP) {
       if (row_ok) {
@@ -167,20 +183,10 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
     const int tok = row_ok ? (tok_lds != nullptr ? tok_lds[t_loc] : a.tokens[tg]) : -1;
     const int tl = (tok >= 0) ? (int)((int64_t)tok - vlane) : -1000000;
     if constexpr (NV == 2) {
-      if (tl >= 0 && tl < 128 && (tl & 15) < 4) {
-        float zf = 0.f;
-#pragma unroll
-        for (int i = 0; i < 32; ++i)
-          if ((i >> 2) * 16 + (i & 3) == tl) zf = z[i];
-        zt_l[t_loc] = zf;
-      }
+      if (tl >= 0 && tl < 128 && (tl & 15) < 4) zt_l[t_loc] = select_entry(z, tl);
     } else {
       float zf = 0.f;
-      if (tl >= 0 && tl < 128 && (tl & 15) < 4) {
-#pragma unroll
-        for (int i = 0; i < 32; ++i)
-          if ((i >> 2) * 16 + (i & 3) == tl) zf = z[i];
-      }
+      if (tl >= 0 && tl < 128 && (tl & 15) < 4) zf = select_entry(z, tl);
       // the half's Partial, with the token's logit from the lane holding it
       // (lane group ((token - v0) % 16) / 4 of the row's four)
       const int64_t th = (int64_t)tok - v0;

@@ -180,8 +180,12 @@ struct TileOps {
 };
 
 // Per-lane byte offsets of this wave's DMA loads, relative to the tile's
-// first row at hidden index 0. They do not change along the hidden dimension:
-// each stage only moves the scalar offset.
+// first row at hidden index 0. They do not change along the hidden dimension
+// (each stage only moves the scalar offset) nor from tile to tile (the tile is
+// the buffer resource's base), so one plan serves the whole pass. Rows past an
+// operand's end (a tail tile) lie outside its resource's range, checked on
+// these per-lane offsets, so their loads return zeros: entries the epilogue
+// masks (past V) or rows it never writes (past the batch).
 template <int NTB, int WT, int NV = 2>
 struct LoadPlan {
   static constexpr int NW = Tile<NTB, WT, NV>::NW;
@@ -193,25 +197,33 @@ struct LoadPlan {
 };
 
 template <int NTB, int WT, int NV = 2>
-__device__ __forceinline__ LoadPlan<NTB, WT, NV> make_load_plan(int w_rows, int h_rows, int d, int wave, int lane) {
+__device__ __forceinline__ LoadPlan<NTB, WT, NV> make_load_plan(int d, int wave, int lane) {
   LoadPlan<NTB, WT, NV> pl;
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT, NV>::WB; ++q) {
     const int p = (wave * LoadPlan<NTB, WT, NV>::WB + q) * 64 + lane;
-    int r = p / kChunks;
+    const int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
-    if (r >= w_rows) r = w_rows - 1;  // rows past V: a valid row, masked in the epilogue
     pl.w_off[q] = (uint32_t)(r * d + c * 8) * 2u;
   }
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT, NV>::HB; ++q) {
     const int p = (wave * LoadPlan<NTB, WT, NV>::HB + q) * 64 + lane;
-    int r = p / kChunks;
+    const int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
-    if (r >= h_rows) r = h_rows - 1;  // rows past the batch: never written out
     pl.h_off[q] = (uint32_t)(r * d + c * 8) * 2u;
   }
   return pl;
+}
+
+// This lane's index in its wave, counted afresh at each use rather than kept
+// live across the pass (where register pressure would spill it, and a spill's
+// reload waits for every DMA load in flight): the mask goes through an empty
+// asm, so the count cannot be hoisted out of a loop.
+__device__ __forceinline__ int lane_index() {
+  unsigned m = ~0u;
+  asm volatile("" : "+s"(m));
+  return (int)__builtin_amdgcn_mbcnt_hi(m, __builtin_amdgcn_mbcnt_lo(m, 0u));
 }
 
 // Buffer resource over [base, base + bytes): loads outside it return zeros.
@@ -344,19 +356,16 @@ template <int NTB, int WT, int NV = 2>
 struct TileCtx {
   int vt;
   int64_t v0, t0;
-  LoadPlan<NTB, WT, NV> pl;
   rsrc_t wr, hr, tr, cr;
 };
 
 template <int NTB, int WT, int GV, int NV = 2>
-__device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int lid, int n_vt, int n_tt, int wave,
-                                                          int lane) {
+__device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int lid, int n_vt, int n_tt) {
   constexpr int BT = Tile<NTB, WT, NV>::BT;
   constexpr int TA = Tile<NTB, WT, NV>::TA;
-  // Opaque copies: every call recomputes its context instead of the compiler
+  // Opaque copy: every call recomputes its context instead of the compiler
   // reusing (and keeping live) the result of an earlier call.
   asm volatile("" : "+s"(lid));
-  asm volatile("" : "+v"(lane));
   TileCtx<NTB, WT, NV> c;
   int tt;
   tile_of_lid<GV>(lid, n_vt, n_tt, c.vt, tt);
@@ -364,7 +373,6 @@ __device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int 
   c.t0 = (int64_t)tt * BT;
   const int w_rows = (o.a_rows - c.v0) < TA ? (int)(o.a_rows - c.v0) : TA;
   const int h_rows = (o.b_rows - c.t0) < BT ? (int)(o.b_rows - c.t0) : BT;
-  c.pl = make_load_plan<NTB, WT, NV>(w_rows, h_rows, o.K, wave, lane);
   c.wr = make_rsrc((const __bf16*)o.a + c.v0 * o.K, (uint64_t)w_rows * o.K * 2);
   c.hr = make_rsrc((const __bf16*)o.b + c.t0 * o.K, (uint64_t)h_rows * o.K * 2);
   c.tr = make_rsrc(o.tokens + c.t0, (uint64_t)h_rows * 4);
@@ -424,7 +432,6 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   int par = 0;
   const TileOps ops = E::ops(a);
 
-  const int lane0 = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wv = NV == 2 ? (wave & 1) : 0, wt = wave / NV;
 
@@ -442,17 +449,19 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   const int nk_q = nk / 4;     // stages per quarter (SPLITK4)
   constexpr int kStep = kKS * 2;
 
-  TC cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, start + j, n_vt, n_tt, wave, lane0);
+  TC cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, start + j, n_vt, n_tt);
+  const LP pl = make_load_plan<NTB, WT, NV>(ops.K, wave, lane_index());
 
   // prologue: the tile's row data and stages 0 .. kNBuf - 1
   auto prologue = [&]() {
-    if constexpr (kCoefLds) request_coef<BT>(coef_slot + par * BT, cur.cr, wave, lane0);
-    if constexpr (kTokLds) request_tokens<BT>(tok_slot + par * BT, cur.tr, wave, lane0);
+    const int lane_p = lane_index();
+    if constexpr (kCoefLds) request_coef<BT>(coef_slot + par * BT, cur.cr, wave, lane_p);
+    if constexpr (kTokLds) request_tokens<BT>(tok_slot + par * BT, cur.tr, wave, lane_p);
 #pragma unroll
     for (int s = 0; s < kNBuf; ++s)
 #pragma unroll
       for (int q = 0; q < L; ++q)
-        request_load<NTB, WT, NV>(lds + s * SB, cur.wr, cur.hr, cur.pl, wave, (s < nk ? s : nk - 1) * kStep, q);
+        request_load<NTB, WT, NV>(lds + s * SB, cur.wr, cur.hr, pl, wave, (s < nk ? s : nk - 1) * kStep, q);
     wait_vmem<(kNBuf - 1) * L>();  // stage 0 (and the row data) landed
     __syncthreads();
   };
@@ -467,10 +476,8 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
   while (true) {
     // Per-tile lane arithmetic is recomputed inside the loop rather than
     // hoisted out of it (which would keep it live across the whole loop and
-    // push the epilogue into spills): the empty asm hides that the lane index
-    // is loop-invariant.
-    int lane = lane0;
-    asm volatile("" : "+v"(lane));
+    // push the epilogue into spills).
+    const int lane = lane_index();
     // The next tile's context is rebuilt where it is needed (cheap integer
     // work) rather than kept live across the loop.
     const bool has_next = j + w_x < t_x;
@@ -488,10 +495,10 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     for (; k + kNBuf < nk; ++k) {
       unsigned char* cb = lds + (k % kNBuf) * SB;
       region_a_prio();
-      kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, 0, cb, 1, wave, wv, wt, lane);
+      kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, pl, 0, cb, 1, wave, wv, wt, lane);
       wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, cur.pl, (k + kNBuf) * kStep,
+      kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, pl, (k + kNBuf) * kStep,
                                    lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
@@ -502,13 +509,13 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     // through the epilogue), to this tile's own stages again. Stage k sits in
     // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
     {
-      const TC nx = make_tile<NTB, WT, E::kGroupA, NV>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt, wave, lane);
+      const TC nx = make_tile<NTB, WT, E::kGroupA, NV>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt);
 #pragma unroll
       for (int t = 0; t < kNBuf; ++t) {
         k = nk - kNBuf + t;
         unsigned char* cb = lds + t * SB;
         region_a_prio();
-        kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, 0, cb, 1, wave, wv, wt, lane);
+        kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, pl, 0, cb, 1, wave, wv, wt, lane);
         wait_lgkm0_vmem<(kNBuf - 2) * L>();
         stage_barrier();
         // request k + kNBuf: stage t of the next tile (with its row data)
@@ -517,10 +524,10 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
           if constexpr (kTokLds) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
         }
         if (t + 1 < kNBuf)
-          kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds + (t + 1) * SB, 0,
+          kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep, lds + (t + 1) * SB, 0,
                                        wave, wv, wt, lane);
         else
-          kstep<NTB, WT, 1, kAD, true, false, NV>(fa, fb, acc, cb, nx.wr, nx.hr, nx.pl, t * kStep, lds, 0, wave, wv,
+          kstep<NTB, WT, 1, kAD, true, false, NV>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep, lds, 0, wave, wv,
                                               wt, lane);
         if constexpr (SPLITK4) {
           if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
@@ -543,7 +550,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     par ^= 1;
     if (!has_next) break;
     j += w_x;
-    cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, next_lid, n_vt, n_tt, wave, lane);
+    cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, next_lid, n_vt, n_tt);
     if constexpr (!kSep) {
       __syncthreads();  // the epilogue's reads of the first buffer are done
       prologue();
