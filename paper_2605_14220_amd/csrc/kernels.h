@@ -98,7 +98,8 @@ int n_half_tiles(int V);
 // row tile of one workgroup; it changes the launch shape only.
 hipError_t launch_partials(const LmHeadArgs& a, int rows_per_wg, bool splitk4, hipStream_t s);
 // Partials of every (row, half vocabulary tile), 64 or 128 rows per row tile
-// (by the launch's row count): part is [rows, n_half_tiles]; each half's
+// (by the launch's row count; 2 or 4 waves of 128 x 32): part is
+// [rows, n_half_tiles]; each half's
 // partial equals the one the whole-tile epilogue merges, so
 // launch_merge_halves gives the outputs of launch_partials + launch_merge bit
 // for bit.
@@ -108,7 +109,8 @@ hipError_t launch_partials_halves(const LmHeadArgs& a, hipStream_t s);
 // three per CU) whose last round of workgroups leaves fewer slots idle; the
 // half shape re-reads the row tile once per 128 vocabulary entries instead of
 // 256, so it only pays where it evens out the rounds. 65..128 rows: always
-// (whole tiles one per CU against halves two). Either gives the same bits.
+// (whole tiles one workgroup per CU against halves two, each of four waves).
+// Either gives the same bits.
 bool prefer_half_tiles(int V, int64_t rows);
 hipError_t launch_merge_halves(const Partial* part, const int32_t* tokens, int64_t rows, int V, float* logp,
                                float* entropy, float* lse, hipStream_t s);

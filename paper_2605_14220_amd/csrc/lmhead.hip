@@ -267,11 +267,11 @@ void lmhead_partials(LmHeadArgs a, int n_vt, int n_tt) {
 }
 
 // Softmax partials of every (half vocabulary tile, row tile), for decode
-// batches: one vocab wave per workgroup, a third of the LDS of a CU each, so
-// that three workgroups share a CU and the vocabulary's 2 * ceil(V / 256)
-// halves fill the chip more evenly than its ceil(V / 256) tiles at two per CU.
-// A half's partial is the one the whole-tile epilogue forms for that half
-// before merging the two.
+// batches: one vocab wave per workgroup along the vocabulary (WT waves along
+// the rows), a third or half of the LDS of a CU each, so that several
+// workgroups share a CU and the vocabulary's 2 * ceil(V / 256) halves fill the
+// chip more evenly than its ceil(V / 256) tiles. A half's partial is the one
+// the whole-tile epilogue forms for that half before merging the two.
 // (PER_CU workgroups of WT waves put up to ceil(PER_CU * WT / 4) waves on
 // one SIMD, which bounds each wave's registers.)
 template <int NTB, int WT>
@@ -435,7 +435,8 @@ static double round_fill(int64_t units, int64_t slots) {
 
 bool prefer_half_tiles(int V, int64_t rows) {
   // 65..128 rows: whole tiles of this row tile run one workgroup per CU,
-  // halves two, which measured faster at every vocabulary size tried
+  // halves two (four waves each), which measured faster at every vocabulary
+  // size tried
   if (rows > 64) return true;
   const int cus = device_cu_count();
   if (cus <= 0) return false;
@@ -444,21 +445,22 @@ bool prefer_half_tiles(int V, int64_t rows) {
   return round_fill(n_half_tiles(V), half_slots) > round_fill(n_vocab_tiles(V), whole_slots);
 }
 
-template <int NTB>
+template <int NTB, int WT>
 static hipError_t launch_halves_t(const LmHeadArgs& a, hipStream_t s) {
   const int n_ht = n_half_tiles(a.V);
-  constexpr int BT = Tile<NTB, 2, 1>::BT;
+  constexpr int BT = Tile<NTB, WT, 1>::BT;
   const int64_t n_tt = (a.rows + BT - 1) / BT;
   const int64_t nblk = n_tt * n_ht;
   if (nblk > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((lmhead_half_partials<NTB, 2>), dim3((unsigned)nblk), dim3(64 * 2), 0, s, a, n_ht, (int)n_tt);
+  hipLaunchKernelGGL((lmhead_half_partials<NTB, WT>), dim3((unsigned)nblk), dim3(64 * WT), 0, s, a, n_ht, (int)n_tt);
   return hipGetLastError();
 }
 
-// 64-row tiles (three workgroups of 2 waves per CU) up to 64 rows, 128-row
-// tiles (two per CU) above.
+// 64-row tiles (three workgroups of 2 waves of 128 x 32 per CU) up to 64
+// rows, 128-row tiles (two workgroups of 4 waves of 128 x 32 per CU: two waves
+// per SIMD) above.
 hipError_t launch_partials_halves(const LmHeadArgs& a, hipStream_t s) {
-  return a.rows <= 64 ? launch_halves_t<1>(a, s) : launch_halves_t<2>(a, s);
+  return a.rows <= 64 ? launch_halves_t<1, 2>(a, s) : launch_halves_t<1, 4>(a, s);
 }
 
 // Launches of at most this many rows merge with four waves per row.

@@ -187,8 +187,8 @@ def test_quad_merge_equals_wave_merge(V):
 
 def test_decode_128_row_tiles_full_size():
     """d = 4096, V = 151936, decode batches of 65..128 rows (the 128-row half
-    tiles): bitwise equal to the training path, and to the oracle on sampled
-    rows."""
+    tiles of four waves): bitwise equal to the training path, and to the
+    oracle on sampled rows."""
     T, d, V = 128, 4096, 151936
     h, W = inputs(T, d, V, seed=46, w_std=0.02)
     tok = _tokens(T, V, seed=46)
@@ -203,6 +203,27 @@ def test_decode_128_row_tiles_full_size():
     check_close("decode-128 logp", trn[0], ref_lp, TOL_LOGP, rows=rows)
     check_close("decode-128 entropy", trn[1], ref_H, TOL_ENT, rows=rows)
 
+
+@pytest.mark.parametrize("d", [128, 384, 640])
+@pytest.mark.parametrize("V", [1, 129, 383, 4096 + 77, 4096 + 200])
+@pytest.mark.parametrize("T", [65, 96, 97, 127, 128])
+def test_decode_65_128_bitwise_equal_training(d, V, T):
+    """Decode batches of 65..128 rows (half tiles of 128 rows, four row waves
+    of 32, some of them empty or cut by the batch) at hidden sizes of 2, 6 and
+    10 stages and every kind of vocabulary tail, each call repeated: bitwise equal
+    to the training path, and within tolerance of the oracle at d = 128."""
+    print(f"case decode 65..128 d={d} V={V} T={T}", flush=True)
+    h, W = inputs(T, d, V, seed=(V + 5 * T + d) % 1000, w_std=0.1)
+    tok = _tokens(T, V, seed=V + 3 * T + d)
+    trn = tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, lse=True)
+    for _ in range(2):
+        dec, per_row = _decode(h, W, tok, 0.7)
+        assert per_row == -(-V // 128)
+        _same(dec, trn)
+    if d == 128:
+        ref_lp, ref_H = oracle_rows(h, W, tok, 0.7)
+        check_close(f"decode 65..128 logp d={d} V={V}", dec[0], ref_lp, TOL_LOGP)
+        check_close(f"decode 65..128 entropy d={d} V={V}", dec[1], ref_H, TOL_ENT)
 
 
 @pytest.mark.parametrize("d", [128, 256, 384, 640])
