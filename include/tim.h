@@ -247,7 +247,8 @@ tim_status tim_mismatch_seq(const float* logp_a, const float* logp_b, int64_t T,
  * workspace  at least tim_logprobs_backward_workspace_size(T, d, V,
  *          micro_batch) bytes, 16-byte aligned: about
  *          2 * d * V_pad + 4 * step * V_pad + 2 * d * step bytes with
- *          V_pad = ceil(V / 256) * 256 and step = min(T, micro_batch).
+ *          V_pad = ceil(V / 256) * 256 and step = min(T, micro_batch) (d and
+ *          step rounded up to multiples of 256 in the first and second terms).
  *
  * Arithmetic: dlogits is formed in fp32 from the recomputed fp32 logits and
  * rounded once to bf16 (round to nearest even); the two products run on bf16

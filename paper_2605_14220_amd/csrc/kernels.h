@@ -45,12 +45,15 @@ struct DlogitsArgs {
   float inv_tau;
   void* dacc;             // bf16 [rows, ld]; entries V .. ld - 1 of a row are written as 0
   int64_t ld;             // a multiple of 256 covering V
+  int32_t packed;         // dacc row-major, or packed (K = ld) over ceil(rows / 256) whole tiles
 };
 
 // Plain tile pass: out[j * ldo + i] = (accumulate ? out[j * ldo + i] : 0)
 // + sum_k A[i][k] B[j][k] in one fp32 accumulation chain per element, K
-// ascending; A bf16 [a_rows, K], B bf16 [b_rows, K] row-major, K a multiple
-// of 128, a_rows a multiple of 4.
+// ascending; A bf16 [a_rows, K] and B bf16 [b_rows, K] in the packed layout
+// (tilepass.h) over whole 256-row tiles (rows padded up to a multiple of 256,
+// the padding's outputs never written), K a multiple of 128, a_rows a
+// multiple of 4.
 struct GemmArgs {
   const void* a;
   const void* b;
@@ -119,10 +122,12 @@ hipError_t launch_merge(const Partial* part, const int32_t* tokens, int64_t rows
                         bool left_fold, float* logp, float* entropy, float* lse, hipStream_t s);
 hipError_t launch_dlogits(const DlogitsArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
-// dst[c * ld_dst + r] = src[r * ld_src + c] for r < R, 0 for R <= r < R_pad,
-// c < C (bf16; C and R_pad multiples of 64, 16-byte aligned rows).
-hipError_t launch_transpose(const void* src, int64_t R, int64_t C, int64_t ld_src, void* dst, int64_t R_pad,
-                            int64_t ld_dst, hipStream_t s);
+// dst[c][r] = src[r][c] for r < R, c < C, and 0 for the rest of r < R_pad,
+// c < C_pad (bf16), dst in the packed layout [C_pad, R_pad] (K = R_pad);
+// src row-major with row stride ld_src, or (src_packed) packed with K =
+// ld_src. C_pad a multiple of 256, R_pad of 64, C of 8; 16-byte aligned rows.
+hipError_t launch_transpose(const void* src, bool src_packed, int64_t R, int64_t C, int64_t ld_src, void* dst,
+                            int64_t R_pad, int64_t C_pad, hipStream_t s);
 // Per-row words (lse, alpha, beta, gamma) of the logit gradient for upstream
 // gradients g (of logp) and e (of the entropy; may be null): with g' = g for
 // a token in [0, V) else 0, alpha = (g' + e H) / tau, beta = e / tau,

@@ -16,7 +16,8 @@
 //   1. lmhead_dlogits: z recomputed with the forward's own main loop (K = d),
 //      so p is formed from exactly the logits whose lse the forward returned;
 //      the epilogue writes dacc as bf16 [rows, V_pad] (the rounding a bf16
-//      trainer applies to logit gradients before the weight products).
+//      trainer applies to logit gradients before the weight products), in the
+//      tile pass's packed layout when it feeds the products.
 //   2. dh = dacc . W: A = W^T [d, V_pad], B = dacc, K = V_pad. A row's chain
 //      runs over the whole padded vocabulary in one order whatever the batch,
 //      so dh is batch-invariant like the forward.
@@ -25,8 +26,12 @@
 //      after the first micro-batch (or with accumulation), so micro-batches of
 //      multiples of 128 tokens continue one chain: dW is bitwise the same for
 //      every such micro-batch size.
-// The transposed operands are written by an LDS-tiled transpose; the padding
-// rows and columns are zeros, which add exactly nothing.
+// The transposed operands are written by an LDS-tiled transpose. Both
+// products read packed operands (256-row tiles stored stage by stage as their
+// LDS image, see tilepass.h), which their producers write at no extra cost:
+// the transposes and the logit-gradient epilogue. The padding along K is
+// zeros, which add exactly nothing; padding rows only reach outputs that are
+// never written.
 
 #include "tilepass.h"
 
@@ -41,11 +46,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Logit gradients. A = W [V, d], B = hidden states, K = d: the forward's pass.
 // For row block bj a lane holds row (l % 16) and, in register r of W block bi,
 // the vocabulary entry v0 + wv * 128 + bi * 16 + 4 (l / 16) + r; the four
-// registers go out as one 8-byte store.
+// registers go out as one 8-byte store, to the row-major or the packed place
+// of those four entries (four consecutive K of one row, inside one chunk).
 struct EpiDlogits {
   using Args = DlogitsArgs;
   static constexpr bool kTokens = true;
   static constexpr bool kCoef = true;
+  static constexpr bool kPacked = false;  // operands W and h as the caller holds them
   static constexpr int kGroupA = kGroupV;
   static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
@@ -80,7 +87,12 @@ struct EpiDlogits {
       const float lse = c[0], alpha = c[1], beta = c[2], gamma = c[3];
       // the token's offset from this lane's first entry (both below 2^31)
       const int tl = tok_lds[t_loc] - (int)vlane;
+      // entry vlane + bi * 16 of row tg: row-major, or packed (tile t0 / 256,
+      // row t_loc of it; stage vlane / 64 + bi / 4, chunk 2 (bi % 4) + g / 2
+      // before the swizzle, its half g % 2)
       uint16_t* row = out + tg * a.ld + vlane;
+      uint16_t* prow = out + (t0 >> 8) * (a.ld << 8) + (vlane >> 6) * (kPackRows * kKS) + t_loc * kKS + 4 * (g & 1);
+      const int psw = swz(t_loc);
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
         float o[4];
@@ -95,7 +107,9 @@ struct EpiDlogits {
           if (!full && bi * 16 + r >= lim) dv = 0.f;
           o[r] = dv;
         }
-        *(uint2*)(row + bi * 16) = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        uint16_t* dst = a.packed ? prow + (bi >> 2) * (kPackRows * kKS) + (((2 * (bi & 3) + (g >> 1)) ^ psw) << 3)
+                                 : row + bi * 16;
+        *(uint2*)dst = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
       }
     }
   }
@@ -104,11 +118,12 @@ struct EpiDlogits {
 // fp32 stores of the tile (optionally continuing from the stored values):
 // lane l holds B row j = t0 + wt * NTB * 32 + bj * 16 + l % 16 and the 4
 // consecutive A rows i = v0 + wv * 128 + bi * 16 + 4 (l / 16) + r, one 16-byte
-// access each.
+// access each. Both operands packed.
 struct EpiStore {
   using Args = GemmArgs;
   static constexpr bool kTokens = false;
   static constexpr bool kCoef = false;
+  static constexpr bool kPacked = true;
   static constexpr int kGroupA = kStoreGroup;
   static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
@@ -167,9 +182,12 @@ void gemm_nt_f32(GemmArgs a, int n_vt, int n_tt) {
 
 // 64 x 64 bf16 tile per workgroup: 16-byte row loads into LDS, then each
 // thread gathers 8 consecutive source rows of one column into one 16-byte
-// store of the destination row.
-__global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict__ src, int64_t R, int64_t ld_src,
-                                                      uint16_t* __restrict__ dst, int64_t ld_dst) {
+// store of the destination row, which is packed [C_pad, R_pad] (K = R_pad).
+// The source is row-major with row stride ld_src, or packed with K = ld_src;
+// entries past R or C read as zeros.
+template <bool SRC_PACKED>
+__global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict__ src, int64_t R, int64_t C,
+                                                      int64_t ld_src, uint16_t* __restrict__ dst, int64_t R_pad) {
   __shared__ uint16_t t[64][66];
   const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
   const int tid = threadIdx.x;
@@ -178,7 +196,8 @@ __global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict
     const int idx = tid + 256 * s;
     const int rr = idx >> 3, cc = (idx & 7) * 8;
     uint4 v = uint4{0u, 0u, 0u, 0u};
-    if (r0 + rr < R) v = *(const uint4*)(src + (r0 + rr) * ld_src + c0 + cc);
+    if (r0 + rr < R && c0 + cc < C)
+      v = *(const uint4*)(src + (SRC_PACKED ? packed_index(r0 + rr, c0 + cc, ld_src) : (r0 + rr) * ld_src + c0 + cc));
     uint32_t* d = (uint32_t*)&t[rr][cc];
     d[0] = v.x;
     d[1] = v.y;
@@ -193,7 +212,7 @@ __global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict
     uint32_t w[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) w[k] = (uint32_t)t[rr + 2 * k][cc] | ((uint32_t)t[rr + 2 * k + 1][cc] << 16);
-    *(uint4*)(dst + (c0 + cc) * ld_dst + r0 + rr) = uint4{w[0], w[1], w[2], w[3]};
+    *(uint4*)(dst + packed_index(c0 + cc, r0 + rr, R_pad)) = uint4{w[0], w[1], w[2], w[3]};
   }
 }
 
@@ -242,13 +261,19 @@ hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   return launch_pass<EpiStore, 2, 4>(gemm_nt_f32<2, 4>, a, a.a_rows, a.b_rows, s);
 }
 
-hipError_t launch_transpose(const void* src, int64_t R, int64_t C, int64_t ld_src, void* dst, int64_t R_pad,
-                            int64_t ld_dst, hipStream_t s) {
-  if (C % 64 != 0 || R_pad % 64 != 0 || R > R_pad) return hipErrorInvalidValue;
-  if (C == 0 || R_pad == 0) return hipSuccess;
-  if (R_pad / 64 > 0x7fffffff || C / 64 > 65535) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(transpose_bf16, dim3((unsigned)(R_pad / 64), (unsigned)(C / 64)), dim3(256), 0, s,
-                     (const uint16_t*)src, R, ld_src, (uint16_t*)dst, ld_dst);
+hipError_t launch_transpose(const void* src, bool src_packed, int64_t R, int64_t C, int64_t ld_src, void* dst,
+                            int64_t R_pad, int64_t C_pad, hipStream_t s) {
+  if (C_pad % kPackRows != 0 || R_pad % kKS != 0 || R > R_pad || C > C_pad || C % 8 != 0) return hipErrorInvalidValue;
+  if (src_packed && (ld_src % kKS != 0 || C > ld_src)) return hipErrorInvalidValue;
+  if (C_pad == 0 || R_pad == 0) return hipSuccess;
+  if (R_pad / 64 > 0x7fffffff || C_pad / 64 > 65535) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(R_pad / 64), (unsigned)(C_pad / 64));
+  if (src_packed)
+    hipLaunchKernelGGL(transpose_bf16<true>, grid, dim3(256), 0, s, (const uint16_t*)src, R, C, ld_src,
+                       (uint16_t*)dst, R_pad);
+  else
+    hipLaunchKernelGGL(transpose_bf16<false>, grid, dim3(256), 0, s, (const uint16_t*)src, R, C, ld_src,
+                       (uint16_t*)dst, R_pad);
   return hipGetLastError();
 }
 

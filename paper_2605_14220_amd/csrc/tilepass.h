@@ -93,6 +93,23 @@ struct Shape {
 // 16 distinct 16-byte bank groups of the 64 banks.
 __device__ __forceinline__ int swz(int r) { return (r >> 1) & (kChunks - 1); }
 
+// Packed operand layout, for operands the library writes itself (the
+// backward's transposed copies and its logit gradients): an operand [R, K]
+// (R a multiple of 256, K of 64) is stored tile by tile of 256 rows and, in a
+// tile, stage by stage, each 256 x 64 block exactly as a stage's DMA lays it
+// out in LDS (row r at r * 128 bytes, its logical 16-byte chunk c at physical
+// chunk c ^ swz(r)). Block (tile i, stage s) starts at element
+// (i * K / 64 + s) * 16384, so a stage of a tile is 32 KB of consecutive
+// bytes and every DMA load of it reads 1 KB of consecutive bytes; the row-major
+// layout's stage reads 128 bytes from each of 256 rows far apart.
+constexpr int kPackRows = 256;
+__device__ __forceinline__ int64_t packed_index(int64_t r, int64_t k, int64_t K) {
+  const int rr = (int)(r & (kPackRows - 1));
+  const int kk = (int)(k & (kKS - 1));
+  const int64_t block = (r / kPackRows) * (K / kKS) + k / kKS;
+  return block * (kPackRows * kKS) + rr * kKS + ((((kk >> 3) ^ swz(rr)) << 3) | (kk & 7));
+}
+
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their maxima): at most N of
 // this wave's vector-memory loads (here: global->LDS DMA) are still in flight.
 template <int N>
@@ -182,10 +199,12 @@ struct TileOps {
 // Per-lane byte offsets of this wave's DMA loads, relative to the tile's
 // first row at hidden index 0. They do not change along the hidden dimension
 // (each stage only moves the scalar offset) nor from tile to tile (the tile is
-// the buffer resource's base), so one plan serves the whole pass. Rows past an
-// operand's end (a tail tile) lie outside its resource's range, checked on
-// these per-lane offsets, so their loads return zeros: entries the epilogue
-// masks (past V) or rows it never writes (past the batch).
+// the buffer resource's base), so one plan serves the whole pass. Row-major
+// operands: rows past an operand's end (a tail tile) lie outside its
+// resource's range, checked on these per-lane offsets, so their loads return
+// zeros: entries the epilogue masks (past V) or rows it never writes (past the
+// batch). Packed operands (PK): the offset is the lane's place in the stage
+// block, which is its place in LDS.
 template <int NTB, int WT, int NV = 2>
 struct LoadPlan {
   static constexpr int NW = Tile<NTB, WT, NV>::NW;
@@ -196,7 +215,7 @@ struct LoadPlan {
   uint32_t h_off[HB];
 };
 
-template <int NTB, int WT, int NV = 2>
+template <int NTB, int WT, int NV = 2, bool PK = false>
 __device__ __forceinline__ LoadPlan<NTB, WT, NV> make_load_plan(int d, int wave, int lane) {
   LoadPlan<NTB, WT, NV> pl;
 #pragma unroll
@@ -204,14 +223,14 @@ __device__ __forceinline__ LoadPlan<NTB, WT, NV> make_load_plan(int d, int wave,
     const int p = (wave * LoadPlan<NTB, WT, NV>::WB + q) * 64 + lane;
     const int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
-    pl.w_off[q] = (uint32_t)(r * d + c * 8) * 2u;
+    pl.w_off[q] = PK ? (uint32_t)p * 16u : (uint32_t)(r * d + c * 8) * 2u;
   }
 #pragma unroll
   for (int q = 0; q < LoadPlan<NTB, WT, NV>::HB; ++q) {
     const int p = (wave * LoadPlan<NTB, WT, NV>::HB + q) * 64 + lane;
     const int r = p / kChunks;
     const int c = (p % kChunks) ^ swz(r);
-    pl.h_off[q] = (uint32_t)(r * d + c * 8) * 2u;
+    pl.h_off[q] = PK ? (uint32_t)p * 16u : (uint32_t)(r * d + c * 8) * 2u;
   }
   return pl;
 }
@@ -359,7 +378,8 @@ struct TileCtx {
   rsrc_t wr, hr, tr, cr;
 };
 
-template <int NTB, int WT, int GV, int NV = 2>
+// PK: packed operands (whole padded tile blocks, all in range).
+template <int NTB, int WT, int GV, int NV = 2, bool PK = false>
 __device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int lid, int n_vt, int n_tt) {
   constexpr int BT = Tile<NTB, WT, NV>::BT;
   constexpr int TA = Tile<NTB, WT, NV>::TA;
@@ -373,8 +393,8 @@ __device__ __forceinline__ TileCtx<NTB, WT, NV> make_tile(const TileOps& o, int 
   c.t0 = (int64_t)tt * BT;
   const int w_rows = (o.a_rows - c.v0) < TA ? (int)(o.a_rows - c.v0) : TA;
   const int h_rows = (o.b_rows - c.t0) < BT ? (int)(o.b_rows - c.t0) : BT;
-  c.wr = make_rsrc((const __bf16*)o.a + c.v0 * o.K, (uint64_t)w_rows * o.K * 2);
-  c.hr = make_rsrc((const __bf16*)o.b + c.t0 * o.K, (uint64_t)h_rows * o.K * 2);
+  c.wr = make_rsrc((const __bf16*)o.a + c.v0 * o.K, (uint64_t)(PK ? TA : w_rows) * o.K * 2);
+  c.hr = make_rsrc((const __bf16*)o.b + c.t0 * o.K, (uint64_t)(PK ? BT : h_rows) * o.K * 2);
   c.tr = make_rsrc(o.tokens + c.t0, (uint64_t)h_rows * 4);
   c.cr = make_rsrc((const unsigned char*)o.coef + c.t0 * 16, (uint64_t)h_rows * 16);
   return c;
@@ -447,10 +467,14 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
 
   const int nk = ops.K / kKS;  // stages per tile; a multiple of kNBuf
   const int nk_q = nk / 4;     // stages per quarter (SPLITK4)
-  constexpr int kStep = kKS * 2;
+  // scalar offset from one stage to the next: along a row, or to the next
+  // packed block (A and B tiles alike)
+  constexpr bool kPK = E::kPacked;
+  static_assert(!kPK || (TL::TA == kPackRows && BT == kPackRows), "packed operands come in 256-row tiles");
+  constexpr int kStep = kPK ? kPackRows * kRowBytes : kRowBytes;
 
-  TC cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, start + j, n_vt, n_tt);
-  const LP pl = make_load_plan<NTB, WT, NV>(ops.K, wave, lane_index());
+  TC cur = make_tile<NTB, WT, E::kGroupA, NV, kPK>(ops, start + j, n_vt, n_tt);
+  const LP pl = make_load_plan<NTB, WT, NV, kPK>(ops.K, wave, lane_index());
 
   // prologue: the tile's row data and stages 0 .. kNBuf - 1
   auto prologue = [&]() {
@@ -509,7 +533,8 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     // through the epilogue), to this tile's own stages again. Stage k sits in
     // buffer k % kNBuf = t, as the stage count is a multiple of kNBuf.
     {
-      const TC nx = make_tile<NTB, WT, E::kGroupA, NV>(ops, (kSep && has_next) ? next_lid : start + j, n_vt, n_tt);
+      const TC nx = make_tile<NTB, WT, E::kGroupA, NV, kPK>(ops, (kSep && has_next) ? next_lid : start + j, n_vt,
+                                                            n_tt);
 #pragma unroll
       for (int t = 0; t < kNBuf; ++t) {
         k = nk - kNBuf + t;
@@ -550,7 +575,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
     par ^= 1;
     if (!has_next) break;
     j += w_x;
-    cur = make_tile<NTB, WT, E::kGroupA, NV>(ops, next_lid, n_vt, n_tt);
+    cur = make_tile<NTB, WT, E::kGroupA, NV, kPK>(ops, next_lid, n_vt, n_tt);
     if constexpr (!kSep) {
       __syncthreads();  // the epilogue's reads of the first buffer are done
       prologue();

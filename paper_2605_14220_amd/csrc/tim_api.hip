@@ -225,6 +225,7 @@ tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_
   a.inv_tau = inv_temperature(temperature);
   a.dacc = dlogits;
   a.ld = (int64_t)tim::n_tiles_of(V) * TIM_VOCAB_TILE;
+  a.packed = 0;
   return hip_status(tim::launch_dlogits(a, stream));
 }
 
@@ -252,8 +253,8 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
   const float inv_tau = inv_temperature(temperature);
   const __bf16* h = (const __bf16*)hidden;
 
-  if (grad_hidden) {  // W^T [d, V_pad], zero columns past V
-    st = hip_status(tim::launch_transpose(w_vocab, V, d, d, wt, l.v_pad, l.v_pad, stream));
+  if (grad_hidden) {  // W^T [d_pad, V_pad] packed, zeros past V and d
+    st = hip_status(tim::launch_transpose(w_vocab, false, V, d, d, wt, l.v_pad, l.d_pad, stream));
     if (st != TIM_OK) return st;
   }
   for (int64_t t0 = 0; t0 < T; t0 += l.step) {
@@ -274,6 +275,7 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
     a.inv_tau = inv_tau;
     a.dacc = dacc;
     a.ld = l.v_pad;
+    a.packed = 1;  // [step_pad, V_pad] packed: the products' operand
     st = hip_status(tim::launch_dlogits(a, stream));
     if (st != TIM_OK) return st;
     if (grad_hidden) {  // dh = dlogits . W over the padded vocabulary
@@ -290,9 +292,10 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
       if (st != TIM_OK) return st;
     }
     if (grad_w) {  // dW (+)= dlogits^T . h over this micro-batch's tokens
-      st = hip_status(tim::launch_transpose(dacc, rows, l.v_pad, l.v_pad, dacct, t_pad, t_pad, stream));
+      // dlogits^T [V_pad, t_pad] and h^T [d_pad, t_pad] packed, zeros past the rows
+      st = hip_status(tim::launch_transpose(dacc, true, rows, l.v_pad, l.v_pad, dacct, t_pad, l.v_pad, stream));
       if (st != TIM_OK) return st;
-      st = hip_status(tim::launch_transpose(h + t0 * d, rows, d, d, ht, t_pad, t_pad, stream));
+      st = hip_status(tim::launch_transpose(h + t0 * d, false, rows, d, d, ht, t_pad, l.d_pad, stream));
       if (st != TIM_OK) return st;
       tim::GemmArgs g;
       g.a = ht;

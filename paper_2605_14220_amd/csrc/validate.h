@@ -131,10 +131,12 @@ inline bool valid_backward_micro_batch(int64_t mb) { return mb == 0 || (mb > 0 &
 constexpr int64_t kMaxBackwardStep = (int64_t)1 << 22;
 
 // Workspace of tim_logprobs_backward, each part 256-byte aligned:
-// row words [step] float4 | W^T bf16 [d, V_pad] | dlogits bf16 [step, V_pad]
-// | dlogits^T bf16 [V_pad, T_pad] | hidden^T bf16 [d, T_pad].
+// row words [step] float4 | W^T bf16 [d_pad, V_pad] | dlogits bf16
+// [step_pad, V_pad] | dlogits^T bf16 [V_pad, T_pad] | hidden^T bf16
+// [d_pad, T_pad], the four bf16 operands in the products' packed layout of
+// whole 256-row tiles (d_pad, step_pad: d, step rounded up to 256).
 struct BackwardLayout {
-  int64_t step, t_pad, v_pad;
+  int64_t step, t_pad, v_pad, d_pad, step_pad;
   size_t coef, wt, dacc, dacct, ht, total;
 };
 
@@ -143,17 +145,19 @@ inline BackwardLayout backward_layout(int64_t T, int32_t d, int32_t V, int64_t m
   l.step = (micro_batch > 0 && micro_batch < T) ? micro_batch : T;
   l.t_pad = round_up(l.step, 128);
   l.v_pad = (int64_t)n_tiles_of(V) * TIM_VOCAB_TILE;
+  l.d_pad = round_up(d, 256);
+  l.step_pad = round_up(l.step, 256);
   size_t off = 0;
   l.coef = off;
   off += align256((size_t)l.step * 16u);
   l.wt = off;
-  off += align256((size_t)d * (size_t)l.v_pad * 2u);
+  off += align256((size_t)l.d_pad * (size_t)l.v_pad * 2u);
   l.dacc = off;
-  off += align256((size_t)l.step * (size_t)l.v_pad * 2u);
+  off += align256((size_t)l.step_pad * (size_t)l.v_pad * 2u);
   l.dacct = off;
   off += align256((size_t)l.v_pad * (size_t)l.t_pad * 2u);
   l.ht = off;
-  off += align256((size_t)d * (size_t)l.t_pad * 2u);
+  off += align256((size_t)l.d_pad * (size_t)l.t_pad * 2u);
   l.total = off;
   return l;
 }

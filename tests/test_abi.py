@@ -305,11 +305,13 @@ def test_python_binding_rejects_cpu_tensors():
 # ---------------------------------------------------------------- backward
 
 def _bwd_size(T, d, V, mb):
+    """Row words, then W^T, dlogits, dlogits^T and h^T in whole 256-row tiles."""
     step = mb if 0 < mb < T else T
     t_pad = -(-step // 128) * 128
     v_pad = -(-V // 256) * 256
     a = lambda x: -(-x // 256) * 256
-    return a(step * 16) + a(2 * d * v_pad) + a(2 * step * v_pad) + a(2 * v_pad * t_pad) + a(2 * d * t_pad)
+    d_pad, step_pad = a(d), a(step)
+    return a(step * 16) + a(2 * d_pad * v_pad) + a(2 * step_pad * v_pad) + a(2 * v_pad * t_pad) + a(2 * d_pad * t_pad)
 
 
 @pytest.mark.parametrize("T,d,V,mb", [(700, 256, 4173, 128), (138564, 4096, 151936, 16384), (1, 128, 1, 0),
