@@ -128,6 +128,47 @@ def test_backward_vs_oracle(T, d, V, tau, mb, entropy):
     _bound_check(f"grad_w T={T} V={V}", gw, dacc.T @ hf, np.abs(dacc).T @ np.abs(hf), t_all)
 
 
+
+@pytest.mark.parametrize("T,d,V,mb", [(1, 384, 1, 0), (129, 384, 255, 128), (300, 384, 257, 128),
+                                      (513, 640, 129, 256)])
+def test_backward_ragged_shapes_vs_oracle(T, d, V, mb):
+    """The products read whole 256-row tiles of packed operands: hidden sizes that leave padding rows in the last
+    tile (384, 640), vocabularies of one entry and around a tile edge, micro-batches that end inside a tile. Both
+    gradients against the oracle within the derived bound."""
+    print(f"case ragged T={T} d={d} V={V} mb={mb}", flush=True)
+    h, W, tok, H, lse, gl, ge = _case(T, d, V, 0.9, seed=5 * T + V + d, bad_tokens=True)
+    gh, gw = tim.logprobs_backward(h, W, tok, lse, gl, 0.9, entropy=H, grad_entropy=ge, micro_batch=mb)
+    torch.cuda.synchronize()
+    if V == 1:  # one entry: p = 1, q = 0, H = 0, so every logit gradient is exactly zero
+        assert (gh == 0).all() and (gw == 0).all()
+        return
+    dacc = _oracle_dacc(h, W, tok, 0.9, gl, ge)
+    hf = oracle.bf16_to_f64(bf16_bits(h))
+    wf = oracle.bf16_to_f64(bf16_bits(W))
+    v_pad = (V + 255) // 256 * 256
+    step = mb if 0 < mb < T else T
+    t_all = sum(-(-min(step, T - t0) // 128) * 128 for t0 in range(0, T, step))
+    _bound_check(f"grad_hidden ragged T={T} d={d} V={V}", gh, dacc @ wf, np.abs(dacc) @ np.abs(wf), v_pad)
+    _bound_check(f"grad_w ragged T={T} d={d} V={V}", gw, dacc.T @ hf, np.abs(dacc).T @ np.abs(hf), t_all)
+
+
+def test_backward_ignores_stale_workspace():
+    """A workspace left full of NaN (bf16 0xFFFF) by earlier work gives bitwise the gradients of a zeroed one: the
+    padding along K is written as zeros by the transposes and the logit-gradient pass, and the padding rows of the
+    last packed tiles (here d = 384 of 512, and micro-batches ending inside a tile) reach only outputs that are
+    never written."""
+    T, d, V, mb = 300, 384, 1000, 128
+    h, W, tok, H, lse, gl, ge = _case(T, d, V, 1.0, seed=15)
+    n = tim.backward_workspace_size(T, d, V, mb)
+    got = []
+    for fill in (255, 0):
+        ws = torch.full((n,), fill, dtype=torch.uint8, device="cuda")
+        got.append(tim.logprobs_backward(h, W, tok, lse, gl, 1.0, entropy=H, grad_entropy=ge, micro_batch=mb,
+                                         workspace=ws))
+    (gh_nan, gw_nan), (gh_zero, gw_zero) = got
+    assert torch.isfinite(gh_nan).all() and torch.isfinite(gw_nan).all()
+    assert bits_equal(gh_nan, gh_zero) and bits_equal(gw_nan, gw_zero)
+
 def test_grad_hidden_is_batch_invariant_and_grad_w_micro_batch_invariant():
     T, d, V, tau = 700, 256, 4173, 0.8
     h, W, tok, H, lse, gl, ge = _case(T, d, V, tau, seed=11)
