@@ -71,6 +71,7 @@ struct EpiDlogits {
   __device__ static void epilogue(const Args& a, int, int, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], float*,
                                   const int* tok_lds, const f32x4* coef_lds, int wave, int lane) {
     constexpr int NJ = 2 * NTB;
+    static_assert(WT * NTB * 32 == kPackRows, "a row tile is one 256-row tile of the packed output");
     const int wv = wave & 1, wt = wave >> 1;
     const int g = lane >> 4, c16 = lane & 15;
     const float inv_tau = a.inv_tau;
