@@ -46,8 +46,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Logit gradients. A = W [V, d], B = hidden states, K = d: the forward's pass.
 // For row block bj a lane holds row (l % 16) and, in register r of W block bi,
 // the vocabulary entry v0 + wv * 128 + bi * 16 + 4 (l / 16) + r; the four
-// registers go out as one 8-byte store, to the row-major or the packed place
-// of those four entries (four consecutive K of one row, inside one chunk).
+// registers go out as one 8-byte store to their row-major place or, packed,
+// two lanes' halves of a 16-byte chunk (eight consecutive K of one row) as one
+// 16-byte store.
 struct EpiDlogits {
   using Args = DlogitsArgs;
   static constexpr bool kTokens = true;
@@ -92,8 +93,8 @@ struct EpiDlogits {
       // row t_loc of it; stage vlane / 64 + bi / 4, chunk 2 (bi % 4) + g / 2
       // before the swizzle, its half g % 2)
       uint16_t* row = out + tg * a.ld + vlane;
-      uint16_t* prow = out + (t0 >> 8) * (a.ld << 8) + (vlane >> 6) * (kPackRows * kKS) + t_loc * kKS + 4 * (g & 1);
       const int psw = swz(t_loc);
+      uint2 pk[8];
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
         float o[4];
@@ -108,9 +109,26 @@ struct EpiDlogits {
           if (!full && bi * 16 + r >= lim) dv = 0.f;
           o[r] = dv;
         }
-        uint16_t* dst = a.packed ? prow + (bi >> 2) * (kPackRows * kKS) + (((2 * (bi & 3) + (g >> 1)) ^ psw) << 3)
-                                 : row + bi * 16;
-        *(uint2*)dst = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        pk[bi] = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        if (!a.packed) *(uint2*)(row + bi * 16) = pk[bi];
+      }
+      if (a.packed) {
+        // Lanes l and l ^ 16 (lane groups g and g ^ 1, the same row) hold the
+        // two halves of one chunk. Each swap exchanges the odd group's block
+        // 2m half with the even group's block 2m + 1 half, so an even group
+        // then holds both halves of its block 2m chunk and an odd group those
+        // of its block 2m + 1 chunk, each written as one 16-byte store. Both
+        // lanes of a pair take the same branch above (same row).
+        const bool odd = (g & 1) != 0;
+        uint16_t* pbase = out + (t0 >> 8) * (a.ld << 8) + (vlane >> 6) * (kPackRows * kKS) + t_loc * kKS;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const auto x0 = __builtin_amdgcn_permlane16_swap(pk[2 * m].x, pk[2 * m + 1].x, false, false);
+          const auto x1 = __builtin_amdgcn_permlane16_swap(pk[2 * m].y, pk[2 * m + 1].y, false, false);
+          const int bi = 2 * m + (odd ? 1 : 0);
+          uint16_t* dst = pbase + (bi >> 2) * (kPackRows * kKS) + (((2 * (bi & 3) + (g >> 1)) ^ psw) << 3);
+          *(uint4*)dst = uint4{x0[0], x1[0], x0[1], x1[1]};
+        }
       }
     }
   }
