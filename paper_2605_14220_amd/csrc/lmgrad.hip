@@ -38,9 +38,12 @@
 namespace tim {
 namespace {
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats rounded to bf16 (round to nearest even), lo in the low half.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const __bf16 a = (__bf16)lo, b = (__bf16)hi;  // round to nearest even
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
 
 // Logit gradients. A = W [V, d], B = hidden states, K = d: the forward's pass.
@@ -48,7 +51,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // the vocabulary entry v0 + wv * 128 + bi * 16 + 4 (l / 16) + r; the four
 // registers go out as one 8-byte store to their row-major place or, packed,
 // two lanes' halves of a 16-byte chunk (eight consecutive K of one row) as one
-// 16-byte store.
+// 16-byte store. Per entry the epilogue spends five VALU operations and one
+// exp: the tail mask only in the tail tile, the token's term only in the lane
+// group that holds it.
 struct EpiDlogits {
   using Args = DlogitsArgs;
   static constexpr bool kTokens = true;
@@ -68,6 +73,34 @@ struct EpiDlogits {
 #pragma unroll
       for (int bj = 0; bj < 2 * NTB; ++bj) acc[bi][bj] = f32x4{};
   }
+  // One row block's gradients as bf16 pairs: every entry -p (alpha + beta q)
+  // (FULL: no entry past V); in the lane group holding the row's token, its
+  // entry then adds gamma, which is gamma - p (alpha + beta q) exactly.
+  template <bool FULL>
+  __device__ static void row_block(const f32x4 (&accj)[8], float inv_tau, float lse, float alpha, float beta,
+                                   float gamma, int tl, int lim, uint2 (&pk)[8]) {
+#pragma unroll
+    for (int bi = 0; bi < 8; ++bi) {
+      float o[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        // z * inv_tau: a multiply by exactly 1 returns z itself (fp32 denormals kept)
+        const float q = accj[bi][r] * inv_tau - lse;
+        const float p = exp2_hw(q * kLog2e);
+        o[r] = -(p * __builtin_fmaf(beta, q, alpha));
+        if (!FULL && bi * 16 + r >= lim) o[r] = 0.f;
+      }
+      if ((unsigned)(tl - bi * 16) < 4u) {
+        // a real branch (taken by one lane group of one row), not selects on every entry
+        asm volatile("" ::: "memory");
+        const int rt = tl - bi * 16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (r == rt) o[r] = gamma + o[r];
+      }
+      pk[bi] = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+    }
+  }
   template <int NTB, int WT>
   __device__ static void epilogue(const Args& a, int, int, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], float*,
                                   const int* tok_lds, const f32x4* coef_lds, int wave, int lane) {
@@ -86,40 +119,23 @@ struct EpiDlogits {
       const int64_t tg = t0 + t_loc;
       if (tg >= a.rows) continue;
       const f32x4 c = coef_lds[t_loc];
-      const float lse = c[0], alpha = c[1], beta = c[2], gamma = c[3];
       // the token's offset from this lane's first entry (both below 2^31)
       const int tl = tok_lds[t_loc] - (int)vlane;
-      // entry vlane + bi * 16 of row tg: row-major, or packed (tile t0 / 256,
-      // row t_loc of it; stage vlane / 64 + bi / 4, chunk 2 (bi % 4) + g / 2
-      // before the swizzle, its half g % 2)
-      uint16_t* row = out + tg * a.ld + vlane;
-      const int psw = swz(t_loc);
+      f32x4 accj[8];
+#pragma unroll
+      for (int bi = 0; bi < 8; ++bi) accj[bi] = acc[bi][bj];
       uint2 pk[8];
-#pragma unroll
-      for (int bi = 0; bi < 8; ++bi) {
-        float o[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float z = acc[bi][bj][r];
-          if (inv_tau != 1.0f) z = z * inv_tau;
-          const float q = z - lse;
-          const float p = exp2_hw(q * kLog2e);
-          const float pw = p * __builtin_fmaf(beta, q, alpha);
-          float dv = (tl == bi * 16 + r) ? gamma - pw : -pw;
-          if (!full && bi * 16 + r >= lim) dv = 0.f;
-          o[r] = dv;
-        }
-        pk[bi] = uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-        if (!a.packed) *(uint2*)(row + bi * 16) = pk[bi];
-      }
+      if (full) row_block<true>(accj, inv_tau, c[0], c[1], c[2], c[3], tl, lim, pk);
+      else row_block<false>(accj, inv_tau, c[0], c[1], c[2], c[3], tl, lim, pk);
       if (a.packed) {
-        // Lanes l and l ^ 16 (lane groups g and g ^ 1, the same row) hold the
-        // two halves of one chunk. Each swap exchanges the odd group's block
-        // 2m half with the even group's block 2m + 1 half, so an even group
-        // then holds both halves of its block 2m chunk and an odd group those
-        // of its block 2m + 1 chunk, each written as one 16-byte store. Both
-        // lanes of a pair take the same branch above (same row).
+        // Packed: tile t0 / 256, row t_loc of it; entry vlane + bi * 16 in stage vlane / 64 + bi / 4, chunk
+        // 2 (bi % 4) + g / 2 before the swizzle, its half g % 2. Lanes l and l ^ 16 (lane groups g and g ^ 1,
+        // the same row) hold the two halves of one chunk. Each swap exchanges the odd group's block 2m half with
+        // the even group's block 2m + 1 half, so an even group then holds both halves of its block 2m chunk and
+        // an odd group those of its block 2m + 1 chunk, each written as one 16-byte store. Both lanes of a pair
+        // take the same branch above (same row).
         const bool odd = (g & 1) != 0;
+        const int psw = swz(t_loc);
         uint16_t* pbase = out + (t0 >> 8) * (a.ld << 8) + (vlane >> 6) * (kPackRows * kKS) + t_loc * kKS;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
@@ -129,6 +145,10 @@ struct EpiDlogits {
           uint16_t* dst = pbase + (bi >> 2) * (kPackRows * kKS) + (((2 * (bi & 3) + (g >> 1)) ^ psw) << 3);
           *(uint4*)dst = uint4{x0[0], x1[0], x0[1], x1[1]};
         }
+      } else {
+        uint16_t* row = out + tg * a.ld + vlane;
+#pragma unroll
+        for (int bi = 0; bi < 8; ++bi) *(uint2*)(row + bi * 16) = pk[bi];
       }
     }
   }
