@@ -52,8 +52,9 @@ struct DlogitsArgs {
 // + sum_k A[i][k] B[j][k] in one fp32 accumulation chain per element, K
 // ascending; A bf16 [a_rows, K] and B bf16 [b_rows, K] in the packed layout
 // (tilepass.h) over whole 256-row tiles (rows padded up to a multiple of 256,
-// the padding's outputs never written), K a multiple of 128, a_rows a
-// multiple of 4.
+// the padding's outputs never written), in 64-deep stage blocks or, with
+// deep, 32-deep ones (then K >= 256); K a multiple of 128, a_rows a multiple
+// of 4. Both forms give the same bits.
 struct GemmArgs {
   const void* a;
   const void* b;
@@ -63,6 +64,7 @@ struct GemmArgs {
   float* out;
   int64_t ldo;
   int32_t accumulate;
+  int32_t deep;
 };
 
 // K3 estimator of the correction ratio r = e^delta (Section 4.1), e^delta - 1
@@ -123,11 +125,12 @@ hipError_t launch_merge(const Partial* part, const int32_t* tokens, int64_t rows
 hipError_t launch_dlogits(const DlogitsArgs& a, hipStream_t s);
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s);
 // dst[c][r] = src[r][c] for r < R, c < C, and 0 for the rest of r < R_pad,
-// c < C_pad (bf16), dst in the packed layout [C_pad, R_pad] (K = R_pad);
-// src row-major with row stride ld_src, or (src_packed) packed with K =
-// ld_src. C_pad a multiple of 256, R_pad of 64, C of 8; 16-byte aligned rows.
+// c < C_pad (bf16), dst in the packed layout [C_pad, R_pad] (K = R_pad) in
+// dst_ks-deep stage blocks (64 or 32); src row-major with row stride ld_src,
+// or (src_packed) packed in 64-deep blocks with K = ld_src. C_pad a multiple
+// of 256, R_pad of 64, C of 8; 16-byte aligned rows.
 hipError_t launch_transpose(const void* src, bool src_packed, int64_t R, int64_t C, int64_t ld_src, void* dst,
-                            int64_t R_pad, int64_t C_pad, hipStream_t s);
+                            int64_t R_pad, int64_t C_pad, int dst_ks, hipStream_t s);
 // Per-row words (lse, alpha, beta, gamma) of the logit gradient for upstream
 // gradients g (of logp) and e (of the entropy; may be null): with g' = g for
 // a token in [0, V) else 0, alpha = (g' + e H) / tau, beta = e / tau,

@@ -173,15 +173,17 @@ struct EpiStore {
   template <int NTB, int WT>
   __device__ static void init(const Args& a, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], int wave, int lane) {
     const int wv = wave & 1, wt = wave >> 1;
-    const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
-    const int64_t lim64 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
-    const int lim = lim64 > 256 ? 256 : (int)lim64;
+    // A rows are int32 (a_rows < 2^31), so this lane's first row and the
+    // distance to the end are formed in 32 bits
+    const int i_lane = (int)v0 + wv * 128 + 4 * (lane >> 4);
+    const int lim0 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
+    const int lim = lim0 > 256 ? 256 : lim0;
 #pragma unroll
     for (int bj = 0; bj < 2 * NTB; ++bj) {
       const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
-        const int64_t i0 = i_lane + bi * 16;
+        const int i0 = i_lane + bi * 16;
         acc[bi][bj] = (a.accumulate && jr < a.b_rows && bi * 16 < lim) ? *(const f32x4*)(a.out + jr * a.ldo + i0)
                                                                      : f32x4{};
       }
@@ -191,16 +193,18 @@ struct EpiStore {
   __device__ static void epilogue(const Args& a, int, int, int64_t v0, int64_t t0, f32x4 (&acc)[8][2 * NTB], float*,
                                   const int*, const f32x4*, int wave, int lane) {
     const int wv = wave & 1, wt = wave >> 1;
-    const int64_t i_lane = v0 + wv * 128 + 4 * (lane >> 4);
-    const int64_t lim64 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
-    const int lim = lim64 > 256 ? 256 : (int)lim64;
+    // A rows are int32 (a_rows < 2^31), so this lane's first row and the
+    // distance to the end are formed in 32 bits
+    const int i_lane = (int)v0 + wv * 128 + 4 * (lane >> 4);
+    const int lim0 = a.a_rows - i_lane;  // A rows past the end: bi * 16 >= lim
+    const int lim = lim0 > 256 ? 256 : lim0;
 #pragma unroll
     for (int bj = 0; bj < 2 * NTB; ++bj) {
       const int64_t jr = t0 + wt * NTB * 32 + bj * 16 + (lane & 15);
       if (jr >= a.b_rows) continue;
 #pragma unroll
       for (int bi = 0; bi < 8; ++bi) {
-        const int64_t i0 = i_lane + bi * 16;
+        const int i0 = i_lane + bi * 16;
         if (bi * 16 < lim) *(f32x4*)(a.out + jr * a.ldo + i0) = acc[bi][bj];
       }
     }
@@ -219,12 +223,21 @@ void gemm_nt_f32(GemmArgs a, int n_vt, int n_tt) {
   tile_pass<NTB, WT, false, EpiStore>(a, n_vt, n_tt);
 }
 
+// The same product on operands packed in 32-deep blocks, five stage buffers
+// (one workgroup per CU): the weight gradient's short-K passes.
+constexpr int kDeepBufs = 5;
+template <int NTB, int WT>
+__global__ __launch_bounds__(128 * WT, 1)
+void gemm_nt_f32_deep(GemmArgs a, int n_vt, int n_tt) {
+  tile_pass_deep<NTB, WT, kDeepBufs, EpiStore>(a, n_vt, n_tt);
+}
+
 // 64 x 64 bf16 tile per workgroup: 16-byte row loads into LDS, then each
 // thread gathers 8 consecutive source rows of one column into one 16-byte
-// store of the destination row, which is packed [C_pad, R_pad] (K = R_pad).
-// The source is row-major with row stride ld_src, or packed with K = ld_src;
-// entries past R or C read as zeros.
-template <bool SRC_PACKED>
+// store of the destination row, which is packed [C_pad, R_pad] (K = R_pad) in
+// DST_KS-deep stage blocks. The source is row-major with row stride ld_src, or
+// packed (64-deep blocks) with K = ld_src; entries past R or C read as zeros.
+template <bool SRC_PACKED, int DST_KS>
 __global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict__ src, int64_t R, int64_t C,
                                                       int64_t ld_src, uint16_t* __restrict__ dst, int64_t R_pad) {
   __shared__ uint16_t t[64][66];
@@ -251,7 +264,7 @@ __global__ __launch_bounds__(256) void transpose_bf16(const uint16_t* __restrict
     uint32_t w[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) w[k] = (uint32_t)t[rr + 2 * k][cc] | ((uint32_t)t[rr + 2 * k + 1][cc] << 16);
-    *(uint4*)(dst + packed_index(c0 + cc, r0 + rr, R_pad)) = uint4{w[0], w[1], w[2], w[3]};
+    *(uint4*)(dst + packed_index<DST_KS>(c0 + cc, r0 + rr, R_pad)) = uint4{w[0], w[1], w[2], w[3]};
   }
 }
 
@@ -297,22 +310,24 @@ hipError_t launch_dlogits(const DlogitsArgs& a, hipStream_t s) {
 
 hipError_t launch_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.b_rows <= 0 || a.a_rows <= 0) return hipSuccess;
+  if (a.deep) {  // 32-deep stages: a multiple of 4 of them, at least kDeepBufs + 1
+    if (a.K % 128 != 0 || a.K / 32 < kDeepBufs + 1) return hipErrorInvalidValue;
+    return launch_pass<EpiStore, 2, 4>(gemm_nt_f32_deep<2, 4>, a, a.a_rows, a.b_rows, s);
+  }
   return launch_pass<EpiStore, 2, 4>(gemm_nt_f32<2, 4>, a, a.a_rows, a.b_rows, s);
 }
 
 hipError_t launch_transpose(const void* src, bool src_packed, int64_t R, int64_t C, int64_t ld_src, void* dst,
-                            int64_t R_pad, int64_t C_pad, hipStream_t s) {
-  if (C_pad % kPackRows != 0 || R_pad % kKS != 0 || R > R_pad || C > C_pad || C % 8 != 0) return hipErrorInvalidValue;
+                            int64_t R_pad, int64_t C_pad, int dst_ks, hipStream_t s) {
+  if (dst_ks != 64 && dst_ks != 32) return hipErrorInvalidValue;
+  if (C_pad % kPackRows != 0 || R_pad % 64 != 0 || R > R_pad || C > C_pad || C % 8 != 0) return hipErrorInvalidValue;
   if (src_packed && (ld_src % kKS != 0 || C > ld_src)) return hipErrorInvalidValue;
   if (C_pad == 0 || R_pad == 0) return hipSuccess;
   if (R_pad / 64 > 0x7fffffff || C_pad / 64 > 65535) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(R_pad / 64), (unsigned)(C_pad / 64));
-  if (src_packed)
-    hipLaunchKernelGGL(transpose_bf16<true>, grid, dim3(256), 0, s, (const uint16_t*)src, R, C, ld_src,
-                       (uint16_t*)dst, R_pad);
-  else
-    hipLaunchKernelGGL(transpose_bf16<false>, grid, dim3(256), 0, s, (const uint16_t*)src, R, C, ld_src,
-                       (uint16_t*)dst, R_pad);
+  auto kernel = src_packed ? (dst_ks == 64 ? transpose_bf16<true, 64> : transpose_bf16<true, 32>)
+                           : (dst_ks == 64 ? transpose_bf16<false, 64> : transpose_bf16<false, 32>);
+  hipLaunchKernelGGL(kernel, grid, dim3(256), 0, s, (const uint16_t*)src, R, C, ld_src, (uint16_t*)dst, R_pad);
   return hipGetLastError();
 }
 

@@ -95,19 +95,28 @@ __device__ __forceinline__ int swz(int r) { return (r >> 1) & (kChunks - 1); }
 
 // Packed operand layout, for operands the library writes itself (the
 // backward's transposed copies and its logit gradients): an operand [R, K]
-// (R a multiple of 256, K of 64) is stored tile by tile of 256 rows and, in a
-// tile, stage by stage, each 256 x 64 block exactly as a stage's DMA lays it
-// out in LDS (row r at r * 128 bytes, its logical 16-byte chunk c at physical
-// chunk c ^ swz(r)). Block (tile i, stage s) starts at element
-// (i * K / 64 + s) * 16384, so a stage of a tile is 32 KB of consecutive
-// bytes and every DMA load of it reads 1 KB of consecutive bytes; the row-major
-// layout's stage reads 128 bytes from each of 256 rows far apart.
+// (R a multiple of 256, K of KS) is stored tile by tile of 256 rows and, in a
+// tile, stage by stage, each 256 x KS block exactly as a stage's DMA lays it
+// out in LDS (row r at r * 2 KS bytes, its logical 16-byte chunk c at physical
+// chunk c ^ swz_ks<KS>(r)). Block (tile i, stage s) starts at element
+// (i * K / KS + s) * 256 KS, so a stage of a tile is 512 KS bytes of
+// consecutive memory and every DMA load of it reads 1 KB of consecutive bytes;
+// the row-major layout's stage reads 2 KS bytes from each of 256 rows far
+// apart. KS = 64 for the two-buffer tile pass, 32 for the deep pass below.
 constexpr int kPackRows = 256;
+// With 2 KS-byte rows, a ds_read_b128's 16 consecutive rows at one logical
+// chunk land in 16 distinct 16-byte bank groups: rows 2 apart (KS = 64) or 4
+// apart (KS = 32) share a bank line and take different chunks.
+template <int KS>
+__device__ __forceinline__ int swz_ks(int r) {
+  return KS == 64 ? swz(r) : (r >> 2) & 3;
+}
+template <int KS = kKS>
 __device__ __forceinline__ int64_t packed_index(int64_t r, int64_t k, int64_t K) {
   const int rr = (int)(r & (kPackRows - 1));
-  const int kk = (int)(k & (kKS - 1));
-  const int64_t block = (r / kPackRows) * (K / kKS) + k / kKS;
-  return block * (kPackRows * kKS) + rr * kKS + ((((kk >> 3) ^ swz(rr)) << 3) | (kk & 7));
+  const int kk = (int)(k & (KS - 1));
+  const int64_t block = (r / kPackRows) * (K / KS) + k / KS;
+  return block * (kPackRows * KS) + rr * KS + ((((kk >> 3) ^ swz_ks<KS>(rr)) << 3) | (kk & 7));
 }
 
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt left at their maxima): at most N of
@@ -580,6 +589,194 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
       __syncthreads();  // the epilogue's reads of the first buffer are done
       prologue();
     }
+  }
+  wait_vmem<0>();  // no global->LDS request may outlive the workgroup
+}
+
+// Deep pipeline for packed operands in 32-deep stages (packed_index<32>).
+// The arithmetic is tile_pass's -- the same MFMA, the same operands per lane,
+// K in the same ascending 32-element k-steps, so the same bits -- staged
+// differently: a stage is one k-step (16 KB per 256-row operand tile) and NB
+// buffers keep up to NB - 1 stages in flight, a prefetch lead of about NB - 1.5
+// k-steps against about 1.5 for tile_pass's two 64-deep buffers, at the cost
+// of a barrier per k-step instead of per two. Each stage boundary: every wave
+// waits for its own reads of stage k (issued during k-step k - 1) and its own
+// DMA of stage k + 1, the barrier makes stage k + 1 visible and frees stage
+// k's buffer, which the k-step then refills with stage k + NB while it reads
+// stage k + 1's operands. Used for 256 x 256 tiles of eight waves.
+template <int NTB, int WT>
+struct DeepTile {
+  static constexpr int NW = 2 * WT;
+  static constexpr int NJ = 2 * NTB;
+  static constexpr int BT = WT * NTB * 32;
+  static constexpr int kRow = 64;                     // bytes of a row in a stage
+  static constexpr int kWB = kPackRows * kRow;        // A block of a stage
+  static constexpr int SB = (kPackRows + BT) * kRow;  // stage bytes
+  static constexpr int WB = kWB / (1024 * NW);        // 1 KB DMA loads per wave per stage, A
+  static constexpr int HB = BT * kRow / (1024 * NW);  // and B
+  static constexpr int L = WB + HB;
+};
+
+// Load q of a wave's stage request: the lane's 16 bytes at its place in the
+// stage block (which is its place in LDS), A blocks first.
+template <int NTB, int WT>
+__device__ __forceinline__ void deep_load(unsigned char* buf, rsrc_t wr, rsrc_t hr, int wave, int lane, int soff, int q) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  using DT = DeepTile<NTB, WT>;
+  if (q < DT::WB) {
+    const int blk = wave * DT::WB + q;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void*)(buf + blk * 1024), 16, (uint32_t)(blk * 64 + lane) * 16u,
+                                             soff, 0, 0);
+  } else {
+    const int blk = wave * DT::HB + (q - DT::WB);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(hr, (lds_void*)(buf + DT::kWB + blk * 1024), 16,
+                                             (uint32_t)(blk * 64 + lane) * 16u, soff, 0, 0);
+  }
+#endif
+}
+
+// MFMA operand of a 16-row block from a 32-deep stage: lane l reads row
+// (l % 16) at hidden offset 8 (l / 16) of the stage.
+__device__ __forceinline__ bf16x8 deep_read(const unsigned char* base, int row, int lane) {
+  const int c = (lane >> 4) ^ swz_ks<32>(row);
+  return *(const bf16x8*)(base + row * 64 + c * 16);
+}
+
+// One k-step: MFMA unit i (A block i / NJ, B block i % NJ) with the operands
+// of parity P, its share of the stage request into `lb` (LOAD), and (READ)
+// the next stage's operands from `rb`: the B blocks into the other parity
+// set, each A block into its own register right after its last use here.
+template <int NTB, int WT, int P, bool READ>
+__device__ __forceinline__ void deep_kstep(bf16x8 (&fa)[8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
+                                           unsigned char* lb, rsrc_t wr, rsrc_t hr, int soff, const unsigned char* rb,
+                                           int wave, int wv, int wt, int lane) {
+  using DT = DeepTile<NTB, WT>;
+  constexpr int NJ = DT::NJ;
+  constexpr int NM = 8 * NJ;
+  constexpr int L = DT::L;
+  static_assert(L <= NM, "at most one DMA load per unit");
+#pragma unroll
+  for (int i = 0; i < NM; ++i) {
+    const int bi = i / NJ, bj = i % NJ;
+    acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[bi], fb[P][bj], acc[bi][bj], 0, 0, 0);
+    const int q = (i * L + NM - 1) / NM;  // load q goes with unit q * NM / L
+    if (q < L && q * NM / L == i) deep_load<NTB, WT>(lb, wr, hr, wave, lane, soff, q);
+    if (READ) {
+      if (i < NJ) fb[P ^ 1][i] = deep_read(rb + DT::kWB, wt * NTB * 32 + i * 16 + (lane & 15), lane);
+      if (bj == NJ - 1) fa[bi] = deep_read(rb, wv * 128 + bi * 16 + (lane & 15), lane);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The boundary before k-step k and the k-step: refill buffer bk (stage k's)
+// with the request (wr, hr, soff) and read stage k + 1 from the next buffer.
+template <int NTB, int WT, int NB, int P, bool READ>
+__device__ __forceinline__ void deep_step(bf16x8 (&fa)[8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
+                                          unsigned char* lds, int& bk, rsrc_t wr, rsrc_t hr, int soff, int wave,
+                                          int wv, int wt, int lane) {
+  using DT = DeepTile<NTB, WT>;
+  wait_lgkm0_vmem<(NB - 2) * DT::L>();
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  int bn = bk + 1;
+  if (bn == NB) bn = 0;
+  deep_kstep<NTB, WT, P, READ>(fa, fb, acc, lds + bk * DT::SB, wr, hr, soff, lds + bn * DT::SB, wave, wv, wt, lane);
+  bk = bn;
+}
+
+// Tile pass over packed operands in 32-deep stages, NB stage buffers (global
+// stage g in buffer g % NB); the tile walk and epilogue policy as in
+// tile_pass (the policy's operands packed, no per-row data, no LDS scratch).
+// The stage count ops.K / 32 must be a multiple of 4 and at least NB + 1.
+template <int NTB, int WT, int NB, class E>
+__device__ __forceinline__ void tile_pass_deep(const typename E::Args& a, int n_vt, int n_tt) {
+  using DT = DeepTile<NTB, WT>;
+  using TC = TileCtx<NTB, WT, 2>;
+  constexpr int NJ = DT::NJ;
+  constexpr int SB = DT::SB;
+  constexpr int L = DT::L;
+  constexpr int kStep = kPackRows * DT::kRow;  // from one packed block to the next
+  static_assert(E::kPacked && !E::kTokens && !E::kCoef && E::template scratch_bytes<DT::BT>() == 0,
+                "packed operands, no per-row data, no epilogue scratch");
+  static_assert(DT::BT == kPackRows, "256-row tiles");
+  static_assert(NB * SB <= 160 * 1024, "stage buffers within the LDS");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[NB * SB];
+  const TileOps ops = E::ops(a);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wv = wave & 1, wt = wave >> 1;
+  // this workgroup's tiles: start + wi, start + wi + w_x, ... below start + t_x
+  const int n_tiles = n_vt * n_tt;
+  const int x = blockIdx.x & 7, wi = blockIdx.x >> 3;
+  const int w_x = (int)(gridDim.x >> 3) + (x < (int)(gridDim.x & 7) ? 1 : 0);
+  const int tq = n_tiles >> 3, trm = n_tiles & 7;
+  const int t_x = tq + (x < trm ? 1 : 0);
+  const int start = x * tq + (x < trm ? x : trm);
+  int j = wi;
+  if (j >= t_x) return;
+  const int nk = ops.K / 32;
+
+  TC cur = make_tile<NTB, WT, E::kGroupA, 2, true>(ops, start + j, n_vt, n_tt);
+  {  // prologue: stages 0 .. NB - 1
+    const int lane_p = lane_index();
+#pragma unroll
+    for (int st = 0; st < NB; ++st)
+#pragma unroll
+      for (int q = 0; q < L; ++q) deep_load<NTB, WT>(lds + st * SB, cur.wr, cur.hr, wave, lane_p, st * kStep, q);
+    wait_vmem<(NB - 1) * L>();  // stage 0 landed
+    __syncthreads();
+  }
+  int bk = 0;  // buffer of the current stage
+  f32x4 acc[8][NJ];
+  bf16x8 fa[8];
+  bf16x8 fb[2][NJ];
+  // the last TL stages (TL even, at least NB: their requests may reach the
+  // next tile) run unrolled with the operand parity known
+  constexpr int TL = (NB + 1) & ~1;
+  while (true) {
+    const int lane = lane_index();
+    const bool has_next = j + w_x < t_x;
+    const int next_lid = start + j + w_x;
+    E::template init<NTB, WT>(a, cur.v0, cur.t0, acc, wave, lane);
+    {  // stage 0 has landed and is visible
+      const unsigned char* b0 = lds + bk * SB;
+#pragma unroll
+      for (int bj = 0; bj < NJ; ++bj) fb[0][bj] = deep_read(b0 + DT::kWB, wt * NTB * 32 + bj * 16 + (lane & 15), lane);
+#pragma unroll
+      for (int bi = 0; bi < 8; ++bi) fa[bi] = deep_read(b0, wv * 128 + bi * 16 + (lane & 15), lane);
+    }
+    int k = 0;
+    for (; k + TL < nk; k += 2) {  // every request is a stage of this tile
+      deep_step<NTB, WT, NB, 0, true>(fa, fb, acc, lds, bk, cur.wr, cur.hr, (k + NB) * kStep, wave, wv, wt, lane);
+      deep_step<NTB, WT, NB, 1, true>(fa, fb, acc, lds, bk, cur.wr, cur.hr, (k + 1 + NB) * kStep, wave, wv, wt,
+                                      lane);
+    }
+    {  // requests past the tile go to the next tile's first stages, or, with
+       // none, re-read this tile's
+      const TC nx = make_tile<NTB, WT, E::kGroupA, 2, true>(ops, has_next ? next_lid : start + j, n_vt, n_tt);
+#pragma unroll
+      for (int t = 0; t < TL; ++t) {
+        const int kn = k + t + NB;
+        const bool in_tile = kn < nk;
+        const int soff = (in_tile ? kn : kn - nk) * kStep;
+        const rsrc_t wr = in_tile ? cur.wr : nx.wr;
+        const rsrc_t hr = in_tile ? cur.hr : nx.hr;
+        if (t + 1 < TL) {
+          if (t & 1) deep_step<NTB, WT, NB, 1, true>(fa, fb, acc, lds, bk, wr, hr, soff, wave, wv, wt, lane);
+          else deep_step<NTB, WT, NB, 0, true>(fa, fb, acc, lds, bk, wr, hr, soff, wave, wv, wt, lane);
+        } else {
+          deep_step<NTB, WT, NB, 1, false>(fa, fb, acc, lds, bk, wr, hr, soff, wave, wv, wt, lane);
+        }
+      }
+    }
+    E::template epilogue<NTB, WT>(a, n_vt, cur.vt, cur.v0, cur.t0, acc, nullptr, nullptr, nullptr, wave,
+                                  lane_index());
+    if (!has_next) break;
+    j += w_x;
+    cur = make_tile<NTB, WT, E::kGroupA, 2, true>(ops, next_lid, n_vt, n_tt);
   }
   wait_vmem<0>();  // no global->LDS request may outlive the workgroup
 }

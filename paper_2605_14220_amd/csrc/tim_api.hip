@@ -254,7 +254,7 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
   const __bf16* h = (const __bf16*)hidden;
 
   if (grad_hidden) {  // W^T [d_pad, V_pad] packed, zeros past V and d
-    st = hip_status(tim::launch_transpose(w_vocab, false, V, d, d, wt, l.v_pad, l.d_pad, stream));
+    st = hip_status(tim::launch_transpose(w_vocab, false, V, d, d, wt, l.v_pad, l.d_pad, 64, stream));
     if (st != TIM_OK) return st;
   }
   for (int64_t t0 = 0; t0 < T; t0 += l.step) {
@@ -288,14 +288,19 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
       g.out = grad_hidden + t0 * d;
       g.ldo = d;
       g.accumulate = 0;
+      g.deep = 0;
       st = hip_status(tim::launch_gemm(g, stream));
       if (st != TIM_OK) return st;
     }
     if (grad_w) {  // dW (+)= dlogits^T . h over this micro-batch's tokens
-      // dlogits^T [V_pad, t_pad] and h^T [d_pad, t_pad] packed, zeros past the rows
-      st = hip_status(tim::launch_transpose(dacc, true, rows, l.v_pad, l.v_pad, dacct, t_pad, l.v_pad, stream));
+      // dlogits^T [V_pad, t_pad] and h^T [d_pad, t_pad] packed, zeros past the rows; in 32-deep stage blocks
+      // for the deep pass (its five buffers hide the HBM latency of this short-K product) when the pass
+      // has at least 8 of them, else in 64-deep ones
+      const bool deep = t_pad >= 256;
+      const int ks = deep ? 32 : 64;
+      st = hip_status(tim::launch_transpose(dacc, true, rows, l.v_pad, l.v_pad, dacct, t_pad, l.v_pad, ks, stream));
       if (st != TIM_OK) return st;
-      st = hip_status(tim::launch_transpose(h + t0 * d, false, rows, d, d, ht, t_pad, l.d_pad, stream));
+      st = hip_status(tim::launch_transpose(h + t0 * d, false, rows, d, d, ht, t_pad, l.d_pad, ks, stream));
       if (st != TIM_OK) return st;
       tim::GemmArgs g;
       g.a = ht;
@@ -306,6 +311,7 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
       g.out = grad_w;
       g.ldo = d;
       g.accumulate = (accumulate_grad_w || t0 > 0) ? 1 : 0;
+      g.deep = deep ? 1 : 0;
       st = hip_status(tim::launch_gemm(g, stream));
       if (st != TIM_OK) return st;
     }
