@@ -152,6 +152,26 @@ def test_backward_ragged_shapes_vs_oracle(T, d, V, mb):
     _bound_check(f"grad_w ragged T={T} d={d} V={V}", gw, dacc.T @ hf, np.abs(dacc).T @ np.abs(hf), t_all)
 
 
+
+def test_backward_maximum_vocabulary():
+    """The largest vocabulary the boundary accepts (V = 2048 * 256: 2048 vocabulary tiles, the widest packed A
+    operand of grad_hidden and B operand of grad_w): grad_hidden on every row and grad_w on 64 seeded vocabulary rows
+    plus every token's row against the oracle, within the derived bound."""
+    T, d, V, tau = 9, 128, 2048 * 256, 1.1
+    h, W, tok, H, lse, gl, ge = _case(T, d, V, tau, seed=17)
+    gh, gw = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H, grad_entropy=ge)
+    torch.cuda.synchronize()
+    dacc = _oracle_dacc(h, W, tok, tau, gl, ge)
+    wf = oracle.bf16_to_f64(bf16_bits(W))
+    hf = oracle.bf16_to_f64(bf16_bits(h))
+    _bound_check("grad_hidden max-vocab", gh, dacc @ wf, np.abs(dacc) @ np.abs(wf), V)
+    rng = np.random.default_rng(17)
+    vrows = np.unique(np.concatenate([tok.cpu().numpy().astype(np.int64), rng.choice(V, 61, replace=False),
+                                      [0, V - 1, V - 256]]))
+    da = np.ascontiguousarray(dacc[:, vrows])
+    _bound_check("grad_w max-vocab rows", torch.as_tensor(gw.double().cpu().numpy()[vrows]), da.T @ hf,
+                 np.abs(da).T @ np.abs(hf), 128)
+
 def test_backward_ignores_stale_workspace():
     """A workspace left full of NaN (bf16 0xFFFF) by earlier work gives bitwise the gradients of a zeroed one: the
     padding along K is written as zeros by the transposes and the logit-gradient pass, and the padding rows of the

@@ -69,6 +69,24 @@ def test_ragged_shapes_all_rows(T, d, V, tau, mode, mb):
     check_close("lse", lse, ref_lse, TOL_LOGP)
 
 
+
+@pytest.mark.parametrize("V", [2048 * 256, 2048 * 256 - 77])
+def test_maximum_vocabulary_both_modes(V):
+    """The largest vocabulary the boundary accepts (2048 tiles: the merge's widest tree, and 4096 or 4095 halves in
+    a decode batch) and a ragged one just below it: every row against the oracle in both modes, the modes bitwise
+    equal."""
+    T, d = 9, 128
+    print(f"case maximum vocabulary V={V}", flush=True)
+    h, W = inputs(T, d, V, seed=V % 1009, w_std=0.1)
+    tok = random_tokens(T, V, seed=V % 1009)
+    tok[0] = V - 1          # the last entry of the last tile
+    lp_r, H_r, _ = tim.logprobs(h, W, tok, 0.9, mode=Mode.ROLLOUT)
+    lp_t, H_t, _ = tim.logprobs(h, W, tok, 0.9, mode=Mode.TRAINING)
+    assert bits_equal(lp_r, lp_t) and bits_equal(H_r, H_t)
+    ref_lp, ref_H = oracle_rows(h, W, tok, 0.9)
+    check_close(f"max-vocab logp V={V}", lp_r, ref_lp, TOL_LOGP)
+    check_close(f"max-vocab entropy V={V}", H_r, ref_H, TOL_ENT)
+
 @pytest.mark.parametrize("V", [1, 2, 3, 255, 256, 257, 511, 513])
 def test_small_and_ragged_vocab(V):
     T, d = 70, 256
