@@ -87,6 +87,24 @@ def test_maximum_vocabulary_both_modes(V):
     check_close(f"max-vocab logp V={V}", lp_r, ref_lp, TOL_LOGP)
     check_close(f"max-vocab entropy V={V}", H_r, ref_H, TOL_ENT)
 
+
+def test_eight_million_rows_one_call():
+    """A call of 2^23 + 37 rows at d = 128 (one launch of 32769 row tiles in each mode): the hidden block is 2.15 GB,
+    so row offsets pass 2^31 bytes. The modes bitwise equal, sampled rows (the first, the last, both sides of the
+    2^31-byte offset, seeded ones) against the oracle."""
+    T, d, V = 2 ** 23 + 37, 128, 600
+    h, W = inputs(T, d, V, seed=23, w_std=0.1)
+    tok = random_tokens(T, V, seed=23)
+    lp_t, H_t, _ = tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING)
+    lp_r, H_r, _ = tim.logprobs(h, W, tok, 1.0, mode=Mode.ROLLOUT)
+    assert bits_equal(lp_r, lp_t) and bits_equal(H_r, H_t)
+    rng = np.random.default_rng(23)
+    edge = 2 ** 31 // (2 * d)  # the first row at byte offset 2^31
+    rows = np.unique(np.concatenate([[0, 1, 255, 256, edge - 1, edge, T - 38, T - 1], rng.choice(T, 56, replace=False)]))
+    ref_lp, ref_H = oracle_rows(h, W, tok, 1.0, rows=rows)
+    check_close("8M-row logp", lp_t, ref_lp, TOL_LOGP, rows=rows)
+    check_close("8M-row entropy", H_t, ref_H, TOL_ENT, rows=rows)
+
 @pytest.mark.parametrize("V", [1, 2, 3, 255, 256, 257, 511, 513])
 def test_small_and_ragged_vocab(V):
     T, d = 70, 256
