@@ -172,6 +172,29 @@ def test_backward_maximum_vocabulary():
     _bound_check("grad_w max-vocab rows", torch.as_tensor(gw.double().cpu().numpy()[vrows]), da.T @ hf,
                  np.abs(da).T @ np.abs(hf), 128)
 
+
+def test_backward_largest_pass():
+    """A pass of 2^22 - 100 tokens, padded to 2^22 (the largest pass the boundary accepts, and the weight gradient's
+    longest chain: its stage offsets reach 2^31 - 16 KB), gives bitwise the gradients of two passes of 2^21 tokens;
+    grad_hidden on sampled rows against the oracle within the derived bound."""
+    T, d, V, tau = 2 ** 22 - 100, 128, 256, 1.0
+    h, W = inputs(T, d, V, seed=19, w_std=0.1)
+    tok = random_tokens(T, V, 19)
+    lp, H, lse = tim.logprobs(h, W, tok, tau, lse=True)
+    gl, ge = _upstream(T, 19)
+    gh0, gw0 = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H, grad_entropy=ge, micro_batch=0)
+    gh1, gw1 = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H, grad_entropy=ge, micro_batch=2 ** 21)
+    assert bits_equal(gh0, gh1) and bits_equal(gw0, gw1)
+    assert torch.isfinite(gw0).all()
+    rng = np.random.default_rng(19)
+    rows = np.unique(np.concatenate([[0, 2 ** 21 - 1, 2 ** 21, T - 1], rng.choice(T, 60, replace=False)]))
+    idx = torch.as_tensor(rows, device="cuda")
+    hs, ts = h.index_select(0, idx), tok.index_select(0, idx)
+    dacc = oracle.logit_grads(bf16_bits(hs), bf16_bits(W), ts.cpu().numpy(), tau,
+                              gl.index_select(0, idx).cpu().double().numpy(), ge.index_select(0, idx).cpu().double().numpy())
+    wf = oracle.bf16_to_f64(bf16_bits(W))
+    _bound_check("grad_hidden largest pass", gh0.index_select(0, idx), dacc @ wf, np.abs(dacc) @ np.abs(wf), V)
+
 def test_backward_ignores_stale_workspace():
     """A workspace left full of NaN (bf16 0xFFFF) by earlier work gives bitwise the gradients of a zeroed one: the
     padding along K is written as zeros by the transposes and the logit-gradient pass, and the padding rows of the
