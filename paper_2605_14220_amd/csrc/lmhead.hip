@@ -227,9 +227,10 @@ __device__ __forceinline__ void tile_epilogue(const LmHeadArgs& a, int n_vt, int
 }
 
 // Epilogue policies of a tile pass. Each one names the pass's operands (and
-// whether they are in the packed layout), the LDS it needs beside the stage
-// buffers, the per-row data it wants staged in LDS with each tile, how the
-// accumulators start, and what it does with them.
+// whether they are in the packed layout), how the stage loads are placed in a
+// k-step, the LDS it needs beside the stage buffers, the per-row data it wants
+// staged in LDS with each tile, how the accumulators start, and what it does
+// with them.
 //
 // EpiPartials: the LM head forward. A = W [V, d], B = hidden states, K = d;
 // the epilogue forms the tile's softmax partials (or, DUMP, writes logits);
@@ -240,6 +241,7 @@ struct EpiPartials {
   static constexpr bool kTokens = !DUMP;
   static constexpr bool kCoef = false;
   static constexpr bool kPacked = false;  // W and h as the caller holds them
+  static constexpr int kLoadSpacing = 0;  // stage loads spread evenly over a k-step's MFMAs
   static constexpr int kGroupA = kGroupV;
   static constexpr int kNV = NV;
   template <int BT>

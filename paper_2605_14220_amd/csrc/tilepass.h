@@ -324,13 +324,14 @@ __device__ __forceinline__ bf16x8 read_b(const unsigned char* buf, int s, int bj
 // issues the MFMA of W block bi = i / NJ and row block bj = i % NJ (the
 // accumulation order of every logit is the k-step order; the order of the
 // units only interleaves independent chains), then, with LOAD, its share of
-// the DMA loads of a stage request into `lb`, and, with READ, the reads of
-// k-step `rs` of buffer `rb`. Operands alternate between two register sets by
+// the DMA loads of a stage request into `lb` (spread evenly over the units,
+// or with SP > 0 one every SP units from the first), and, with READ, the
+// reads of k-step `rs` of buffer `rb`. Operands alternate between two register sets by
 // k-step parity P: the row-block operands always, read from the first units
 // on; the W operands too with AD (then read right after the row blocks, so
 // every read lands early), else the single W set is refilled block by block
 // right after each block's last use here.
-template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true, int NV = 2>
+template <int NTB, int WT, int P, bool AD, bool LOAD, bool READ = true, int NV = 2, int SP = 0>
 __device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NTB], f32x4 (&acc)[8][2 * NTB],
                                       unsigned char* lb, rsrc_t wr, rsrc_t hr, const LoadPlan<NTB, WT, NV>& pl,
                                       int soff, const unsigned char* rb, int rs, int wave, int wv, int wt, int lane) {
@@ -339,13 +340,18 @@ __device__ __forceinline__ void kstep(bf16x8 (&fa)[2][8], bf16x8 (&fb)[2][2 * NT
   constexpr int L = LoadPlan<NTB, WT, NV>::L;
   constexpr int PA = AD ? P : 0, PN = AD ? (P ^ 1) : 0;
   static_assert(L <= NM, "at most one DMA load per unit");
+  static_assert(SP == 0 || SP * (L - 1) < NM, "the spaced loads fit in the k-step");
 #pragma unroll
   for (int i = 0; i < NM; ++i) {
     const int bi = i / NJ, bj = i % NJ;
     acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[PA][bi], fb[P][bj], acc[bi][bj], 0, 0, 0);
-    if (LOAD) {  // load q goes with unit q * NM / L
-      const int q = (i * L + NM - 1) / NM;
-      if (q < L && q * NM / L == i) request_load<NTB, WT, NV>(lb, wr, hr, pl, wave, soff, q);
+    if (LOAD) {  // load q goes with unit q * NM / L, or q * SP
+      if constexpr (SP > 0) {
+        if (i % SP == 0 && i / SP < L) request_load<NTB, WT, NV>(lb, wr, hr, pl, wave, soff, i / SP);
+      } else {
+        const int q = (i * L + NM - 1) / NM;
+        if (q < L && q * NM / L == i) request_load<NTB, WT, NV>(lb, wr, hr, pl, wave, soff, q);
+      }
     }
     if (READ) {
       if (!AD && i < NJ) fb[P ^ 1][i] = read_b<NTB, NV>(rb, rs, i, wt, lane);
@@ -531,7 +537,7 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
       kstep<NTB, WT, 0, kAD, false, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, pl, 0, cb, 1, wave, wv, wt, lane);
       wait_lgkm0_vmem<(kNBuf - 2) * L>();
       stage_barrier();
-      kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, cur.wr, cur.hr, pl, (k + kNBuf) * kStep,
+      kstep<NTB, WT, 1, kAD, true, true, NV, E::kLoadSpacing>(fa, fb, acc, cb, cur.wr, cur.hr, pl, (k + kNBuf) * kStep,
                                    lds + ((k + 1) % kNBuf) * SB, 0, wave, wv, wt, lane);
       if constexpr (SPLITK4) {
         if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
@@ -558,10 +564,12 @@ __device__ __forceinline__ void tile_pass(const typename E::Args& a, int n_vt, i
           if constexpr (kTokLds) request_tokens<BT>(tok_slot + (par ^ 1) * BT, nx.tr, wave, lane);
         }
         if (t + 1 < kNBuf)
-          kstep<NTB, WT, 1, kAD, true, true, NV>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep, lds + (t + 1) * SB, 0,
+          kstep<NTB, WT, 1, kAD, true, true, NV, E::kLoadSpacing>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep,
+                                                                  lds + (t + 1) * SB, 0,
                                        wave, wv, wt, lane);
         else
-          kstep<NTB, WT, 1, kAD, true, false, NV>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep, lds, 0, wave, wv,
+          kstep<NTB, WT, 1, kAD, true, false, NV, E::kLoadSpacing>(fa, fb, acc, cb, nx.wr, nx.hr, pl, t * kStep, lds,
+                                                                   0, wave, wv,
                                               wt, lane);
         if constexpr (SPLITK4) {
           if ((k + 1) % nk_q == 0) quarter_fold<NTB>(acc, sum, (k + 1) / nk_q - 1);
