@@ -62,7 +62,9 @@ struct EpiDlogits {
   // stage loads one every 3 MFMAs from the k-step's start (2% faster here than
   // spread evenly, which stays faster for the forward)
   static constexpr int kLoadSpacing = 3;
-  static constexpr int kGroupA = kGroupV;
+  // vocab tiles per group of its tile order: 2 (1-2% faster here than the
+  // forward's 4; 1 and 8 slower)
+  static constexpr int kGroupA = 2;
   static constexpr int kNV = 2;  // vocab waves: whole 256-entry A tiles
   template <int BT>
   static constexpr int scratch_bytes() { return 0; }
