@@ -46,6 +46,11 @@ struct DlogitsArgs {
   void* dacc;             // bf16 [rows, ld]; entries V .. ld - 1 of a row are written as 0
   int64_t ld;             // a multiple of 256 covering V
   int32_t packed;         // dacc row-major, or packed (K = ld) over ceil(rows / 256) whole tiles
+  // Optional (null: none): the same gradients transposed, bf16 [ld, t_pad] packed in 32-deep stage blocks
+  // (K = t_pad), the weight gradient's operand; token rows rows .. t_pad - 1 are written as 0. With it, dacc may
+  // be null (no [rows, ld] image written).
+  void* dacct;
+  int64_t t_pad;          // rows rounded up to a multiple of 128, at least 256 (used with dacct)
 };
 
 // Plain tile pass: out[j * ldo + i] = (accumulate ? out[j * ldo + i] : 0)

@@ -226,6 +226,8 @@ tim_status tim_logit_grads(const void* hidden, const void* w_vocab, const int32_
   a.dacc = dlogits;
   a.ld = (int64_t)tim::n_tiles_of(V) * TIM_VOCAB_TILE;
   a.packed = 0;
+  a.dacct = nullptr;
+  a.t_pad = 0;
   return hip_status(tim::launch_dlogits(a, stream));
 }
 
@@ -264,6 +266,11 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
                                           grad_entropy ? grad_entropy + t0 : nullptr, tokens + t0, rows, V,
                                           temperature, coef, stream));
     if (st != TIM_OK) return st;
+    // dlogits^T [V_pad, t_pad] and h^T [d_pad, t_pad] packed, zeros past the rows; in 32-deep stage blocks for
+    // the deep pass (its five buffers hide the HBM latency of this short-K product) when the pass has at least
+    // 8 of them, else in 64-deep ones. On the deep pass the logit-gradient epilogue writes dlogits^T itself.
+    const bool deep = t_pad >= 256;
+    const int ks = deep ? 32 : 64;
     tim::DlogitsArgs a;
     a.hidden = h + t0 * d;
     a.w = w_vocab;
@@ -273,9 +280,11 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
     a.d = d;
     a.V = V;
     a.inv_tau = inv_tau;
-    a.dacc = dacc;
+    a.dacc = (grad_hidden || !deep) ? dacc : nullptr;
     a.ld = l.v_pad;
     a.packed = 1;  // [step_pad, V_pad] packed: the products' operand
+    a.dacct = (grad_w && deep) ? dacct : nullptr;
+    a.t_pad = t_pad;
     st = hip_status(tim::launch_dlogits(a, stream));
     if (st != TIM_OK) return st;
     if (grad_hidden) {  // dh = dlogits . W over the padded vocabulary
@@ -293,13 +302,10 @@ tim_status tim_logprobs_backward(const void* hidden, const void* w_vocab, const 
       if (st != TIM_OK) return st;
     }
     if (grad_w) {  // dW (+)= dlogits^T . h over this micro-batch's tokens
-      // dlogits^T [V_pad, t_pad] and h^T [d_pad, t_pad] packed, zeros past the rows; in 32-deep stage blocks
-      // for the deep pass (its five buffers hide the HBM latency of this short-K product) when the pass
-      // has at least 8 of them, else in 64-deep ones
-      const bool deep = t_pad >= 256;
-      const int ks = deep ? 32 : 64;
-      st = hip_status(tim::launch_transpose(dacc, true, rows, l.v_pad, l.v_pad, dacct, t_pad, l.v_pad, ks, stream));
-      if (st != TIM_OK) return st;
+      if (!deep) {
+        st = hip_status(tim::launch_transpose(dacc, true, rows, l.v_pad, l.v_pad, dacct, t_pad, l.v_pad, ks, stream));
+        if (st != TIM_OK) return st;
+      }
       st = hip_status(tim::launch_transpose(h + t0 * d, false, rows, d, d, ht, t_pad, l.d_pad, ks, stream));
       if (st != TIM_OK) return st;
       tim::GemmArgs g;

@@ -118,6 +118,10 @@ def test_backward_vs_oracle(T, d, V, tau, mb, entropy):
     h, W, tok, H, lse, gl, ge = _case(T, d, V, tau, seed=3 * T + V, entropy=entropy, bad_tokens=True)
     gh, gw = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H if entropy else None, grad_entropy=ge,
                                    micro_batch=mb)
+    # grad_w alone (the logit-gradient pass then writes only the weight pass's operand) gives the same bits
+    _, gw_only = tim.logprobs_backward(h, W, tok, lse, gl, tau, entropy=H if entropy else None, grad_entropy=ge,
+                                       micro_batch=mb, want_hidden=False)
+    assert bits_equal(gw_only, gw)
     torch.cuda.synchronize()
     dacc = _oracle_dacc(h, W, tok, tau, gl, ge)
     hf = oracle.bf16_to_f64(bf16_bits(h))
@@ -195,12 +199,15 @@ def test_backward_largest_pass():
     wf = oracle.bf16_to_f64(bf16_bits(W))
     _bound_check("grad_hidden largest pass", gh0.index_select(0, idx), dacc @ wf, np.abs(dacc) @ np.abs(wf), V)
 
-def test_backward_ignores_stale_workspace():
+@pytest.mark.parametrize("mb", [128, 256, 0])
+def test_backward_ignores_stale_workspace(mb):
     """A workspace left full of NaN (bf16 0xFFFF) by earlier work gives bitwise the gradients of a zeroed one: the
     padding along K is written as zeros by the transposes and the logit-gradient pass, and the padding rows of the
     last packed tiles (here d = 384 of 512, and micro-batches ending inside a tile) reach only outputs that are
-    never written."""
-    T, d, V, mb = 300, 384, 1000, 128
+    never written. Micro-batches of 128 take the transpose of the logit gradients; one pass of 300 (padded to 384)
+    has the logit-gradient pass write them transposed itself, token rows 300..383 as zeros; 256 + 44 takes one
+    of each."""
+    T, d, V = 300, 384, 1000
     h, W, tok, H, lse, gl, ge = _case(T, d, V, 1.0, seed=15)
     n = tim.backward_workspace_size(T, d, V, mb)
     got = []
