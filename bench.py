@@ -41,6 +41,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (256 CUs x 2.4 GHz)
+
+
+def launch_slices(T: int, mb: int, lr: int):
+    """Row ranges of the training launches: micro-batches of mb rows, each in launches of at most lr rows (the
+    library's planner, tim_logprobs_rows_per_launch), exactly as tim_logprobs runs them."""
+    out = []
+    for m0 in range(0, T, mb):
+        m1 = min(T, m0 + mb)
+        out += [(a, min(m1, a + lr)) for a in range(m0, m1, lr)]
+    return out
 PEAK_HBM_GBS = 8000.0
 METRIC = "tokens/s fused LM-head logp+entropy (d=4096,V=151936); % bf16 MFMA peak"
 
@@ -271,7 +281,8 @@ def other_workload(name, steps, decode_rows=0):
     tok = sample_tokens(h, W, tau, uniforms(T, us), dtype=torch.float32)
     ws_buf = torch.empty(tim.workspace_size(T, d, V, Mode.TRAINING, mb), dtype=torch.uint8, device=dev)
     out = tuple(torch.empty(T, dtype=torch.float32, device=dev) for _ in range(3))
-    slices = [(i * mb, min(T, (i + 1) * mb)) for i in range((T + mb - 1) // mb)]
+    lr = tim.rows_per_launch(T, d, Mode.TRAINING, mb)
+    slices = launch_slices(T, mb, lr)
     stream = torch.cuda.current_stream(dev)
 
     def step(evs):
@@ -295,16 +306,16 @@ def other_workload(name, steps, decode_rows=0):
     t1.record(stream)
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    full = [e0.elapsed_time(e1) for evs in allev for (a, b), (e0, e1) in zip(slices, evs) if b - a == mb]
+    full = [e0.elapsed_time(e1) for evs in allev for (a, b), (e0, e1) in zip(slices, evs) if b - a == lr]
     k_ms = float(np.mean(full))
-    k_frac = 2.0 * d * V * mb / (k_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS
+    k_frac = 2.0 * d * V * lr / (k_ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS
     r = {"workload": f"{name}: d={d} V={V} {cfg.n_responses} responses U[{cfg.len_lo},{cfg.len_hi}] packed = {T} "
                      f"tokens, training mode, micro-batch {mb}, tau={tau}",
          "tokens": T, "steps": steps, "ms_per_step": ms, "tokens_per_s": T / (ms / 1e3),
          "mfma_peak_frac": 2.0 * d * V * T / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS,
-         "partials_launch_ms": k_ms, "partials_rows_per_launch": mb, "partials_frac": k_frac}
+         "partials_launch_ms": k_ms, "partials_rows_per_launch": lr, "partials_frac": k_frac}
     log(f"[bench] {name}: {ms:.3f} ms/step, {r['tokens_per_s']:,.0f} tokens/s = {r['mfma_peak_frac']:.1%} of bf16 "
-        f"peak; partials kernel {k_ms:.3f} ms per {mb}-row launch = {k_frac:.1%}")
+        f"peak; partials kernel {k_ms:.3f} ms per {lr}-row launch = {k_frac:.1%}")
     if decode_rows:
         B = decode_rows
         rws = torch.empty(tim.workspace_size(B, d, V, Mode.ROLLOUT), dtype=torch.uint8, device=dev)
@@ -430,7 +441,6 @@ def main(argv=None):
     log(f"[bench] {cfg.name}: T={T} d={d} V={V} tau={tau} micro_batch={mb}; inputs ready in "
         f"{time.perf_counter() - t_gen:.1f}s")
 
-    n_mb = (T + mb - 1) // mb
     ws_buf = torch.empty(tim.workspace_size(T, d, V, Mode.TRAINING, mb), dtype=torch.uint8, device=dev)
     logp = torch.empty(T, dtype=torch.float32, device=dev)
     ent = torch.empty(T, dtype=torch.float32, device=dev)
@@ -439,7 +449,8 @@ def main(argv=None):
     # the second engine's log-probs (split-K4 reduction order), untimed
     logp_b, _, _ = tim.logprobs(h, W, tok, tau, mode=Mode.TRAINING, micro_batch=mb, order=Order.SPLITK4,
                                 workspace=ws_buf)
-    slices = [(i * mb, min(T, (i + 1) * mb)) for i in range(n_mb)]
+    lr = tim.rows_per_launch(T, d, Mode.TRAINING, mb)  # the planner's launches within each micro-batch
+    slices = launch_slices(T, mb, lr)
     stream = torch.cuda.current_stream(dev)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in slices]
 
@@ -488,10 +499,10 @@ def main(argv=None):
     durs = []
     for stepev in kern_ms:
         for (a, b), (e0, e1) in zip(slices, stepev):
-            if b - a == mb:
+            if b - a == lr:
                 durs.append(e0.elapsed_time(e1))
     avg_ms = float(np.mean(durs))
-    flop_per_launch = 2.0 * d * V * mb
+    flop_per_launch = 2.0 * d * V * lr
     achieved_tflops = flop_per_launch / (avg_ms / 1e3) / 1e12
     path_tflops = 2.0 * d * V * tok_per_s / 1e12
     traffic = load_traffic(f"lmhead_partials_{cfg.name}")

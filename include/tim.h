@@ -48,7 +48,8 @@ typedef enum {
  * so their outputs are bitwise equal for any batching of the same rows. */
 typedef enum {
   TIM_MODE_ROLLOUT = 0,  /* one call per decode step: a ragged batch of rows, one launch */
-  TIM_MODE_TRAINING = 1  /* packed token stream, processed in micro-batches of micro_batch rows */
+  TIM_MODE_TRAINING = 1  /* packed token stream, processed in micro-batches of micro_batch rows (each
+                            micro-batch in launches of at most tim_logprobs_rows_per_launch rows) */
 } tim_mode;
 
 /* Reduction order. TIM_ORDER_SPLITK4 is a deliberately different order of the
@@ -67,12 +68,25 @@ typedef enum {
 /* Largest supported vocabulary: 2048 tiles. */
 #define TIM_MAX_VOCAB (2048 * TIM_VOCAB_TILE)
 
+/* Rows tim_logprobs hands to one kernel launch: T in rollout mode; in training
+ * mode min(T, micro_batch) (micro_batch 0 means T), at most
+ * max(8192, floor((224 MiB / (2 d) - 8192) / 8192) * 8192) rows: the largest
+ * multiple of 8192 whose bf16 hidden block, beside the 16384 d bytes of weight
+ * tiles the GPU's eight XCDs stream at once, fits 224 MiB of the 256 MB
+ * memory-side cache (16384 rows at d = 4096, 8192 at d = 5120). A training
+ * micro-batch longer than that runs as consecutive launches; rows are
+ * independent, so no result changes. Callers composing tim_logprobs_partials
+ * and tim_logprobs_merge themselves take the same launches from this. Returns
+ * 0 for T <= 0, d not a positive multiple of 128, a bad mode or
+ * micro_batch < 0. Pure host function. */
+int64_t tim_logprobs_rows_per_launch(int64_t T, int32_t d, int32_t mode, int64_t micro_batch);
+
 /* Bytes of device workspace tim_logprobs needs for these arguments:
- * rows_per_launch * ceil(V / TIM_VOCAB_TILE) * 16, where rows_per_launch is T
- * in rollout mode and min(T, micro_batch) in training mode (micro_batch 0 means
- * T); in rollout mode with T <= 128 (a decode batch, whose partials may be
- * taken over half tiles) T * ceil(V / (TIM_VOCAB_TILE / 2)) * 16. Returns 0 for
- * invalid arguments or T == 0. Pure host function. */
+ * rows_per_launch * ceil(V / TIM_VOCAB_TILE) * 16, with rows_per_launch from
+ * tim_logprobs_rows_per_launch; in rollout mode with T <= 128 (a decode batch,
+ * whose partials may be taken over half tiles)
+ * T * ceil(V / (TIM_VOCAB_TILE / 2)) * 16. Returns 0 for invalid arguments or
+ * T == 0. Pure host function. */
 size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch);
 
 /* Token log-probabilities and entropies of T rows (Section 2, Eq. 1's terms).

@@ -64,6 +64,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         raise ImportError(f"{path} is not built; run `python -m paper_2605_14220_amd.build`")
     lib = ctypes.CDLL(path)
     c = ctypes
+    lib.tim_logprobs_rows_per_launch.restype = c.c_int64
+    lib.tim_logprobs_rows_per_launch.argtypes = [c.c_int64, c.c_int32, c.c_int32, c.c_int64]
     lib.tim_logprobs_workspace_size.restype = c.c_size_t
     lib.tim_logprobs_workspace_size.argtypes = [c.c_int64, c.c_int32, c.c_int32, c.c_int32, c.c_int64]
     lib.tim_logprobs.restype = c.c_int
@@ -138,6 +140,11 @@ def _require_gpu(*tensors):
             raise ValueError("tim: tensors must be on the GPU")
         if t is not None and not t.is_contiguous():
             raise ValueError("tim: tensors must be contiguous")
+
+
+def rows_per_launch(T: int, d: int, mode: Mode = Mode.TRAINING, micro_batch: int = 0) -> int:
+    """Rows tim_logprobs hands to one launch (0 for invalid arguments); see include/tim.h."""
+    return int(load_library().tim_logprobs_rows_per_launch(int(T), int(d), int(mode), int(micro_batch)))
 
 
 def workspace_size(T: int, d: int, V: int, mode: Mode = Mode.TRAINING, micro_batch: int = 0) -> int:

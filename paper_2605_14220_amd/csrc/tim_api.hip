@@ -59,7 +59,7 @@ tim_status run_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
                         float* entropy, float* lse, void* workspace, hipStream_t stream) {
   tim_status st = TIM_OK;
   const bool splitk4 = order == TIM_ORDER_SPLITK4;
-  const int64_t step = tim::rows_per_launch(T, mode, micro_batch);
+  const int64_t step = tim::rows_per_launch(T, d, mode, micro_batch);
   const int tb = row_tile_for(step, mode, splitk4);
   const bool halves = !splitk4 && tim::uses_half_tiles(step, mode) && tim::prefer_half_tiles(V, step);
   const float inv_tau = inv_temperature(temperature);
@@ -98,10 +98,15 @@ tim_status run_logprobs(const void* hidden, const void* w_vocab, const int32_t* 
 
 extern "C" {
 
+int64_t tim_logprobs_rows_per_launch(int64_t T, int32_t d, int32_t mode, int64_t micro_batch) {
+  if (T <= 0 || d <= 0 || d % 128 != 0 || !tim::valid_mode(mode) || micro_batch < 0) return 0;
+  return tim::rows_per_launch(T, d, mode, micro_batch);
+}
+
 size_t tim_logprobs_workspace_size(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch) {
   if (T <= 0 || tim::check_shape(T, d, V, TIM_ORDER_INVARIANT) != TIM_OK) return 0;
   if (!tim::valid_mode(mode) || micro_batch < 0) return 0;
-  return tim::workspace_bytes(T, V, mode, micro_batch);
+  return tim::workspace_bytes(T, d, V, mode, micro_batch);
 }
 
 tim_status tim_logprobs(const void* hidden, const void* w_vocab, const int32_t* tokens, int64_t T,

@@ -28,10 +28,27 @@ inline bool valid_mode(int32_t mode) { return mode == TIM_MODE_ROLLOUT || mode =
 inline bool valid_order(int32_t order) { return order == TIM_ORDER_INVARIANT || order == TIM_ORDER_SPLITK4; }
 inline bool positive_finite(float x) { return std::isfinite(x) && x > 0.f; }
 
-// Rows handed to one launch.
-inline int64_t rows_per_launch(int64_t T, int32_t mode, int64_t micro_batch) {
-  if (mode == TIM_MODE_TRAINING && micro_batch > 0 && micro_batch < T) return micro_batch;
-  return T;
+// Training launches take at most training_launch_cap(d) rows: the largest
+// multiple of 8192 (at least 8192) whose hidden block, beside the weight
+// tiles the eight XCDs stream at once (a group of 4 vocabulary tiles of
+// 256 x d bf16 each: 16384 d bytes), stays within 224 MiB of the 256 MB
+// memory-side cache. 16384 rows at d = 4096, 8192 at d = 5120, 49152 at
+// d = 2048. Rows are independent, so the split changes no result.
+constexpr int64_t kLaunchRowUnit = 8192;
+constexpr int64_t kLaunchCacheBudget = (int64_t)224 << 20;
+inline int64_t training_launch_cap(int32_t d) {
+  const int64_t fit = kLaunchCacheBudget / (2 * (int64_t)d) - kLaunchRowUnit;
+  const int64_t cap = fit / kLaunchRowUnit * kLaunchRowUnit;
+  return cap > kLaunchRowUnit ? cap : kLaunchRowUnit;
+}
+
+// Rows handed to one launch: T in rollout mode; in training mode the
+// micro-batch (T when 0 or larger), at most training_launch_cap(d).
+inline int64_t rows_per_launch(int64_t T, int32_t d, int32_t mode, int64_t micro_batch) {
+  if (mode != TIM_MODE_TRAINING) return T;
+  const int64_t rows = (micro_batch > 0 && micro_batch < T) ? micro_batch : T;
+  const int64_t cap = training_launch_cap(d);
+  return rows > cap ? cap : rows;
 }
 
 // Rollout launches of at most this many rows (decode batches) may form their
@@ -39,8 +56,8 @@ inline int64_t rows_per_launch(int64_t T, int32_t mode, int64_t micro_batch) {
 constexpr int64_t kHalfTileRows = 128;
 inline bool uses_half_tiles(int64_t rows, int32_t mode) { return mode == TIM_MODE_ROLLOUT && rows <= kHalfTileRows; }
 
-inline size_t workspace_bytes(int64_t T, int32_t V, int32_t mode, int64_t micro_batch) {
-  const int64_t rows = rows_per_launch(T, mode, micro_batch);
+inline size_t workspace_bytes(int64_t T, int32_t d, int32_t V, int32_t mode, int64_t micro_batch) {
+  const int64_t rows = rows_per_launch(T, d, mode, micro_batch);
   const int per_row = uses_half_tiles(rows, mode) ? n_half_tiles_of(V) : n_tiles_of(V);
   return (size_t)rows * (size_t)per_row * 16u;
 }
@@ -67,7 +84,7 @@ inline tim_status validate_logprobs(const void* hidden, const void* w, const int
                                     const float* logp, const void* ws, size_t ws_bytes) {
   const tim_status s = validate_logprobs_args(hidden, w, tokens, T, d, V, temperature, mode, micro_batch, order, logp);
   if (s != TIM_OK || T == 0) return s;
-  if (!ws || !aligned16(ws) || ws_bytes < workspace_bytes(T, V, mode, micro_batch))
+  if (!ws || !aligned16(ws) || ws_bytes < workspace_bytes(T, d, V, mode, micro_batch))
     return TIM_ERR_WORKSPACE;
   return TIM_OK;
 }
@@ -80,7 +97,7 @@ inline tim_status validate_logprobs_noalloc(const void* hidden, const void* w, c
                                             const float* logp) {
   const tim_status s = validate_logprobs_args(hidden, w, tokens, T, d, V, temperature, mode, micro_batch, order, logp);
   if (s != TIM_OK || T == 0) return s;
-  if (workspace_bytes(T, V, mode, micro_batch) > TIM_NOALLOC_SCRATCH_BYTES) return TIM_ERR_WORKSPACE;
+  if (workspace_bytes(T, d, V, mode, micro_batch) > TIM_NOALLOC_SCRATCH_BYTES) return TIM_ERR_WORKSPACE;
   return TIM_OK;
 }
 

@@ -39,7 +39,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     assert names == ["tim_logit_grads", "tim_logits", "tim_logprobs", "tim_logprobs_backward",
                      "tim_logprobs_backward_workspace_size", "tim_logprobs_merge", "tim_logprobs_noalloc",
-                     "tim_logprobs_partials",
+                     "tim_logprobs_partials", "tim_logprobs_rows_per_launch",
                      "tim_logprobs_workspace_size", "tim_mismatch", "tim_mismatch_seq", "tim_ppo_loss", "tim_rmsnorm",
                      "tim_rmsnorm_backward", "tim_rmsnorm_backward_workspace_size", "tim_status_string"]
 
@@ -60,6 +60,27 @@ def test_status_strings(lib):
     assert lib.tim_status_string(99).decode() == "unknown tim_status"
 
 
+def _launch_cap(d):
+    # the largest multiple of 8192 rows whose bf16 hidden block plus 16384 d bytes of weight tiles fits 224 MiB
+    return max(8192, (224 * 2 ** 20 // (2 * d) - 8192) // 8192 * 8192)
+
+
+@pytest.mark.parametrize("d,cap", [(4096, 16384), (5120, 8192), (2048, 49152), (8192, 8192), (128, 909312)])
+def test_training_launch_cap(lib, d, cap):
+    assert _launch_cap(d) == cap
+    assert tim.rows_per_launch(10 ** 6, d, Mode.TRAINING, 0) == cap
+    assert tim.rows_per_launch(10 ** 6, d, Mode.TRAINING, 4 * cap) == cap
+    assert tim.rows_per_launch(10 ** 6, d, Mode.TRAINING, cap - 128) == cap - 128
+    assert tim.rows_per_launch(cap - 1, d, Mode.TRAINING, 0) == cap - 1
+    assert tim.rows_per_launch(10 ** 6, d, Mode.ROLLOUT, 4096) == 10 ** 6  # rollout: one launch over all T rows
+
+
+@pytest.mark.parametrize("args", [(0, 4096, 1, 0), (-5, 4096, 1, 0), (10, 100, 1, 0), (10, 0, 1, 0), (10, 4096, 7, 0),
+                                  (10, 4096, 1, -1)])
+def test_rows_per_launch_zero_when_invalid(lib, args):
+    assert lib.tim_logprobs_rows_per_launch(*args) == 0
+
+
 @pytest.mark.parametrize("T,d,V,mode,mb", [
     (64, 256, 4096, Mode.TRAINING, 0),
     (147000, 4096, 151936, Mode.TRAINING, 16384),
@@ -71,9 +92,13 @@ def test_status_strings(lib):
     (5, 128, 1, Mode.ROLLOUT, 0),
     (7, 128, 4096 + 129, Mode.ROLLOUT, 0),
     (131072, 5120, 152064, Mode.TRAINING, 32768),
+    (131072, 5120, 152064, Mode.TRAINING, 0),
+    (138564, 4096, 151936, Mode.TRAINING, 65536),
 ])
 def test_workspace_size_formula(lib, T, d, V, mode, mb):
     rows = T if (mode == Mode.ROLLOUT or mb == 0 or mb >= T) else mb
+    if mode == Mode.TRAINING:  # training launches of at most the cache-fitting row count
+        rows = min(rows, _launch_cap(d))
     # decode batches (rollout, at most 128 rows) keep one partial per half tile
     width = 128 if (mode == Mode.ROLLOUT and rows <= 128) else 256
     assert tim.workspace_size(T, d, V, mode, mb) == rows * math.ceil(V / width) * 16

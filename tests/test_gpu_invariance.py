@@ -74,3 +74,19 @@ def test_repeat_runs_identical(headline):
     h, W, tok, ref = headline
     for _ in range(3):
         _same(tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING, micro_batch=512, lse=True), ref)
+
+
+@pytest.mark.parametrize("d,mb", [(5120, 0), (5120, 20000), (4096, 40000)])
+def test_training_launch_cap_splits_micro_batches(d, mb):
+    """A training micro-batch longer than the planner's launch cap (8192 rows at d = 5120, 16384 at d = 4096) runs as
+    consecutive launches: 8192 + 8192 + 300 rows for 16684 tokens at d = 5120 (one micro-batch, or 16684 / 20000),
+    16384 + 300 at d = 4096. Bitwise the results of one rollout launch over all rows and of 256-row micro-batches."""
+    T = 2 * 8192 + 300 if d == 5120 else 16384 + 300
+    V = 4096
+    h, W = inputs(T, d, V, seed=37)
+    tok = random_tokens(T, V, seed=37)
+    assert tim.rows_per_launch(T, d, Mode.TRAINING, mb) == (8192 if d == 5120 else 16384)
+    assert tim.rows_per_launch(T, d, Mode.ROLLOUT, mb) == T
+    ref = tim.logprobs(h, W, tok, 0.7, mode=Mode.ROLLOUT, lse=True)
+    _same(tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, micro_batch=mb, lse=True), ref)
+    _same(tim.logprobs(h, W, tok, 0.7, mode=Mode.TRAINING, micro_batch=256, lse=True), ref)
