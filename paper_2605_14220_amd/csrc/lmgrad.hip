@@ -138,12 +138,7 @@ struct EpiDlogits {
     const bool full = v0 + kVocabTile <= a.V;
     const int lim = a.V - (int)vlane;  // entries past V: bi * 16 + r >= lim (tail tile only)
     uint16_t* out = (uint16_t*)a.dacc;
-    // Transposed image [ld, t_pad] in 32-deep blocks: after the quad transpose this lane holds entry row
-    // vlane + bi * 16 + (l % 4) of the tile (row rr of its 256, whose chunk swizzle (rr / 4) % 4 is g) and the
-    // four token rows 4 (l % 16 / 4) .. + 3 of the row block.
     const int j4 = lane & 3, qd = c16 >> 2;
-    uint16_t* tbase = (uint16_t*)a.dacct + (v0 >> 8) * (a.t_pad << 8) + (t0 >> 5) * (kPackRows * 32) +
-                      (wv * 128 + 4 * g + j4) * 32 + 4 * (qd & 1);
 #pragma unroll
     for (int bj = 0; bj < NJ; ++bj) {
       const int t_loc = wt * NTB * 32 + bj * 16 + c16;
@@ -158,8 +153,7 @@ struct EpiDlogits {
         for (int bi = 0; bi < 8; ++bi) accj[bi] = acc[bi][bj];
         if (full) row_block<true>(accj, inv_tau, c[0], c[1], c[2], c[3], tl, lim, pk);
         else row_block<false>(accj, inv_tau, c[0], c[1], c[2], c[3], tl, lim, pk);
-        if (!out) {
-        } else if (a.packed) {
+        if (out && a.packed) {
           // Packed: tile t0 / 256, row t_loc of it; entry vlane + bi * 16 in stage vlane / 64 + bi / 4, chunk
           // 2 (bi % 4) + g / 2 before the swizzle, its half g % 2. Lanes l and l ^ 16 (lane groups g and g ^ 1,
           // the same row) hold the two halves of one chunk. Each swap exchanges the odd group's block 2m half
@@ -177,7 +171,7 @@ struct EpiDlogits {
             uint16_t* dst = pbase + (bi >> 2) * (kPackRows * kKS) + (((2 * (bi & 3) + (g >> 1)) ^ psw) << 3);
             *(uint4*)dst = uint4{x0[0], x1[0], x0[1], x1[1]};
           }
-        } else {
+        } else if (out) {
           uint16_t* row = out + tg * a.ld + vlane;
 #pragma unroll
           for (int bi = 0; bi < 8; ++bi) *(uint2*)(row + bi * 16) = pk[bi];
@@ -187,11 +181,13 @@ struct EpiDlogits {
         for (int bi = 0; bi < 8; ++bi) pk[bi] = uint2{0u, 0u};
       }
       if (a.dacct) {
-        // every lane of the quad takes part (rows past the end as zeros); the quad's four token rows lie
-        // together below t_pad or not at all (t_pad is a multiple of 128)
+        // Transposed image [ld, t_pad] in 32-deep blocks: after the quad transpose this lane holds entry row
+        // vlane + bi * 16 + (l % 4) of the tile (row rr of its 256, whose chunk swizzle (rr / 4) % 4 is g) and
+        // the four token rows tq .. tq + 3. Every lane of the quad takes part (rows past the end as zeros); the
+        // quad's four rows lie together below t_pad or not at all (t_pad is a multiple of 128).
         const int tq = (int)t0 + wt * NTB * 32 + bj * 16 + 4 * qd;
-        uint16_t* dst = tbase + (wt * NTB * 32 + bj * 16) / 32 * (kPackRows * 32) +
-                        (((((bj * 16) & 31) >> 3) + (qd >> 1)) ^ g) * 8;
+        uint16_t* dst = (uint16_t*)a.dacct + (v0 >> 8) * (a.t_pad << 8) + (tq >> 5) * (kPackRows * 32) +
+                        (wv * 128 + 4 * g + j4) * 32 + (((((bj * 16) & 31) >> 3) + (qd >> 1)) ^ g) * 8 + 4 * (qd & 1);
         // non-temporal: read back only by the weight pass, after grad_hidden (this pass measured 2.3% faster
         // than with plain stores; the packed stores above stay plain, 1.3% slower non-temporal)
 #pragma unroll
