@@ -138,6 +138,19 @@ def test_stress_invariance_and_mismatch_report():
         out = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=mb, lse=True)
         for x, y in zip(out, ref):
             assert bits_equal(x, y), f"micro-batch {mb} differs"
+    # training micro-batches above 16384 rows run as 16384-row launches at d = 4096; launches of other sizes:
+    # rollout mode's one launch over the whole stream, and a two-stage launch of the first 65536 rows
+    out = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.ROLLOUT, lse=True)
+    for x, y in zip(out, ref):
+        assert bits_equal(x, y), "one launch over the stream differs"
+    n = 65536
+    ws = torch.empty(tim.workspace_size(n, h.shape[1], W.shape[0], Mode.ROLLOUT), dtype=torch.uint8, device="cuda")
+    tim.logprobs_partials(h[:n], W, tok[:n], ws, cfg.temperature, mode=Mode.TRAINING)
+    part = tuple(torch.empty(n, dtype=torch.float32, device="cuda") for _ in range(3))
+    tim.logprobs_merge(ws, tok[:n], W.shape[0], out=part)
+    for x, y in zip(part, ref):
+        assert bits_equal(x, y[:n].contiguous()), "a 65536-row launch differs"
+    del ws
     # rollout: every row once, in shuffled decode batches of random size 1..256
     rng = np.random.default_rng(44)
     perm = torch.as_tensor(rng.permutation(T), device="cuda")
@@ -155,7 +168,8 @@ def test_stress_invariance_and_mismatch_report():
     for x, y in zip(got, ref):
         assert bits_equal(x, y), "rollout groupings differ from training"
     oracle_sample(cfg, h, W, tok, ref[0], ref[1], seed=9)
-    print(f"[stress] {calls} rollout calls + micro-batches 4096/16384/65536: all {T} rows bitwise equal")
+    print(f"[stress] {calls} rollout calls + micro-batches 4096/16384/65536 + launches of {T} and 65536 rows: "
+          f"all {T} rows bitwise equal")
     # second engine: split-K4 reduction order
     eng = tim.logprobs(h, W, tok, cfg.temperature, mode=Mode.TRAINING, micro_batch=16384, order=Order.SPLITK4)
     oracle_sample(cfg, h, W, tok, eng[0], eng[1], seed=8)

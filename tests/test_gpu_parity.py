@@ -89,10 +89,12 @@ def test_maximum_vocabulary_both_modes(V):
 
 
 def test_eight_million_rows_one_call():
-    """A call of 2^23 + 37 rows at d = 128 (one launch of 32769 row tiles in each mode): the hidden block is 2.15 GB,
-    so row offsets pass 2^31 bytes. The modes bitwise equal, sampled rows (the first, the last, both sides of the
-    2^31-byte offset, seeded ones) against the oracle."""
+    """A call of 2^23 + 37 rows at d = 128: in rollout mode one launch of 32769 row tiles over the 2.15 GB hidden
+    block, so row offsets pass 2^31 bytes; in training mode launches of 909312 rows (the planner's cap at d = 128).
+    The modes bitwise equal, sampled rows (the first, the last, both sides of the 2^31-byte offset, seeded ones)
+    against the oracle."""
     T, d, V = 2 ** 23 + 37, 128, 600
+    assert tim.rows_per_launch(T, d, Mode.ROLLOUT) == T and tim.rows_per_launch(T, d, Mode.TRAINING) == 909312
     h, W = inputs(T, d, V, seed=23, w_std=0.1)
     tok = random_tokens(T, V, seed=23)
     lp_t, H_t, _ = tim.logprobs(h, W, tok, 1.0, mode=Mode.TRAINING)
