@@ -730,7 +730,8 @@ def main(argv=None):
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved_tflops / PEAK_BF16_TFLOPS,
                      "traffic": traffic,
-                     "kernel": "lmhead_partials", "launch_ms": avg_ms, "flop_per_launch": flop_per_launch},
+                     "kernel": "lmhead_partials", "launch_ms": avg_ms, "flop_per_launch": flop_per_launch,
+                     "rows_per_launch": lr},
         "cpu_baseline": cpu,
         "cpu_baseline_single_thread": cpu_single,
         "parity_sample": parity,
